@@ -1,0 +1,47 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def _ensure_built():
+    """Build the product library and the oracle only if nothing is built yet
+    (the driver and the GPU machine run the tests on what `build()` produced)."""
+    lib = os.path.join(ROOT, "paper_2507_23387_amd", "libsgemmcube.so")
+    if not os.path.exists(lib):
+        from paper_2507_23387_amd import build
+
+        build.build()
+    if not os.path.exists(os.path.join(ROOT, "oracle", "liboracle.so")):
+        from oracle import build as obuild
+
+        obuild.build()
+
+
+_ensure_built()
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+    config.addinivalue_line("markers", "slow: long-running CPU check")
+
+
+def gpu_available() -> bool:
+    try:
+        import torch
+    except ImportError:
+        return False
+    return torch.cuda.is_available()
+
+
+@pytest.fixture(scope="session")
+def gpu():
+    if not gpu_available():
+        pytest.skip("no GPU visible")
+    import torch
+
+    return torch.device("cuda:0")
