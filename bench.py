@@ -1,0 +1,256 @@
+"""Benchmark: FP32-equivalent throughput of SGEMM-cube on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload c3]
+                    [--order elementwise] [--no-cpu-baseline]
+
+A step is one whole SGEMM-cube call on the named workload (default: the
+8192^3 U[-1,1] peak-throughput case, s = 2^11, elementwise): FP32 A and B
+already resident in HBM -> split (Sec. 3.3) -> three-product MFMA GEMM with
+FP32 reconstruction (Eq. recover_eqn, Sec. 4.5) -> FP32 C in HBM.  It is the
+same work as one sgemm_cube_ws call, issued as its two halves
+(sgemm_cube_prepare + sgemm_cube_compute) so that HIP events on the launch
+stream can time the dominant GEMM kernel inside the timed region.
+
+Prints ONE JSON line.  `value` = 2MNK / t (FP32-equivalent TFLOP/s, Sec. 6.1);
+`roofline` prices the GEMM kernel's 6MNK FP16 MFMA flops against the dense
+FP16 MFMA peak; `cpu_baseline` times the CPU oracle on a bounded row sample of
+the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+METRIC = "FP32-equiv TFLOP/s (2MNK/t) and % of 3-GEMM FP16 MFMA peak; max rel err"
+# MI355X dense FP16 MFMA peak: 256 CU x 2.4 GHz x 4096 FLOP/clk/CU (published
+# as 2.5 PFLOP/s).  The three-GEMM FP32-equivalent peak is a third of it.
+FP16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12
+THREE_GEMM_PEAK_TFLOPS = FP16_PEAK_TFLOPS / 3
+HBM_PEAK_GBS = 8000.0
+GEMM_KERNEL = "gemm_kernel"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    """Hash of the sources the GEMM kernel is built from (ties a committed
+    HBM-traffic measurement to the kernel it was taken on)."""
+    h = hashlib.sha256()
+    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/internal.h"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_entry(workload: str, order: str):
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if data.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return data.get("entries", {}).get(f"{workload}/{order}")
+
+
+def cpu_baseline(A, B, w, scale, order, target_s: float):
+    """Time the oracle (as it stands) on a bounded sample of output rows."""
+    import oracle
+
+    threads = min(len(os.sched_getaffinity(0)), 16)
+    # calibrate on one row per thread, then size the sample to ~target_s
+    rows0 = workloads.sample_rows(w.M, threads, w.seed + 1)
+    t0 = time.perf_counter()
+    oracle.sgemm_rows(A, B, rows0, scale, order, threads=threads)
+    t_cal = time.perf_counter() - t0
+    per_row = t_cal / len(rows0)
+    n = int(max(threads, min(w.M, target_s / max(per_row, 1e-9))))
+    n = max(threads, (n // threads) * threads)
+    rows = workloads.sample_rows(w.M, n, w.seed + 2)
+    t0 = time.perf_counter()
+    oracle.sgemm_rows(A, B, rows, scale, order, threads=threads)
+    t = time.perf_counter() - t0
+    flops = 2.0 * len(rows) * w.N * w.K
+    return {
+        "value": flops / t / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{len(rows)} of {w.M} output rows of {w.name} ({order}, s=2^"
+                  f"{int(np.log2(scale))}), full K={w.K} and N={w.N}; split of all of B "
+                  f"included; {t:.1f} s wall",
+        "seconds": t,
+    }
+
+
+def error_report(C_rows, A, B, rows):
+    """Context errors against an FP64 GEMM on sampled rows (Sec. 6.2 Eq. err
+    plus the componentwise forms)."""
+    ref = A[rows].astype(np.float64) @ B.astype(np.float64)
+    absab = np.abs(A[rows].astype(np.float64)) @ np.abs(B.astype(np.float64))
+    d = np.abs(C_rows.astype(np.float64) - ref)
+    nz = np.abs(ref) > 0
+    return {
+        "max_rel_err": float(np.max(d[nz] / np.abs(ref[nz]))),
+        "max_err_over_absAabsB": float(np.max(d / np.where(absab > 0, absab, 1.0))),
+        "frobenius_rel_err": float(np.linalg.norm(d) / np.linalg.norm(ref)),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c3")
+    ap.add_argument("--order", default=None, help="elementwise | termwise")
+    ap.add_argument("--scale", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-errors", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the method is a "
+              "single-GPU GEMM here and multi-GPU sharding is not built", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2507_23387_amd as sgc
+
+    w = workloads.get(args.workload)
+    order = args.order or w.orders[0]
+    scale = args.scale or w.scales[0]
+    order_code = sgc.binding.ORDERS[order]
+    M, N, K = w.M, w.N, w.K
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    log(f"generating {w.name} ({M}x{N}x{K}, seed {w.seed})")
+    A, B = workloads.workload_operands(w)
+    dA = torch.from_numpy(A).to(dev)
+    dB = torch.from_numpy(B).to(dev)
+    dC = torch.empty((M, N), dtype=torch.float32, device=dev)
+    ws_bytes = sgc.sgemm_cube_workspace_size(M, N, K, order_code)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+
+    def prepare():
+        st = sgc.sgemm_cube_prepare(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, scale,
+                                    ws.data_ptr(), ws_bytes, sh)
+        if st:
+            raise sgc.SgemmCubeError(st, "sgemm_cube_prepare")
+
+    def compute():
+        st = sgc.sgemm_cube_compute(M, N, K, dC.data_ptr(), N, scale, order_code, ws.data_ptr(),
+                                    ws_bytes, sh)
+        if st:
+            raise sgc.SgemmCubeError(st, "sgemm_cube_compute")
+
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        prepare()
+        compute()
+    torch.cuda.synchronize()
+
+    log(f"timing {args.steps} steps")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for s in range(args.steps):
+        ev[s][0].record(stream)
+        prepare()
+        ev[s][1].record(stream)
+        compute()
+        ev[s][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = ev[0][0].elapsed_time(ev[-1][2])
+    split_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    ms_per_step = total_ms / args.steps
+    flops = 2.0 * M * N * K
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    log(f"{ms_per_step:.4f} ms/step (split {split_ms:.4f}, gemm {gemm_ms:.4f}); "
+        f"{value:.1f} TFLOP/s FP32-equivalent = {100 * value / THREE_GEMM_PEAK_TFLOPS:.1f}% "
+        f"of the 3-GEMM peak; wall {wall * 1e3 / args.steps:.4f} ms/step")
+
+    gemm_tflops = 3 * flops / (gemm_ms * 1e-3) / 1e12
+    traffic = traffic_entry(w.name, order)
+    roofline = {
+        "bound": "mfma",
+        "kernel": f"{GEMM_KERNEL} ({order})",
+        "achieved": gemm_tflops,
+        "peak": FP16_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": gemm_tflops / FP16_PEAK_TFLOPS,
+        "traffic": traffic,
+        "algorithmic_flops_per_launch": 3 * flops,
+        "avg_launch_ms": gemm_ms,
+    }
+    split_bytes = 8.0 * (M * K + K * N)  # 4 B read + 2 x 2 B written per element
+    extra = {
+        "pct_of_3gemm_peak": 100 * value / THREE_GEMM_PEAK_TFLOPS,
+        "three_gemm_peak_tflops": THREE_GEMM_PEAK_TFLOPS,
+        "split_ms": split_ms,
+        "split_gbs": split_bytes / (split_ms * 1e-3) / 1e9,
+        "gemm_ms": gemm_ms,
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+    }
+
+    if not args.no_errors:
+        log("context errors on sampled rows vs FP64")
+        rows = workloads.sample_rows(M, 8, w.seed + 3)
+        Cn = dC.cpu().numpy()[rows]
+        extra["errors"] = {order: error_report(Cn, A, B, rows)}
+        Ch = sgc.hgemm(dA, dB)
+        torch.cuda.synchronize()
+        extra["errors"]["hgemm_fp16"] = error_report(Ch.cpu().numpy()[rows], A, B, rows)
+        extra["max_rel_err"] = extra["errors"][order]["max_rel_err"]
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"cpu baseline (oracle) ~{args.cpu_seconds:.0f} s")
+        cpu = cpu_baseline(A, B, w, scale, order, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 MFMA products, f32 accumulation (f32 in/out)",
+        "data": "synthetic",
+        "config": {"workload": w.name, "M": M, "N": N, "K": K, "seed": w.seed,
+                   "distribution": w.dist, "scale": scale, "order": order},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        **extra,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,157 @@
+/*
+ * sgemm_cube.h -- FP32-accuracy GEMM from three FP16 MFMA products on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method (arXiv 2507.23387, "SGEMM-cube"):
+ *   Sec. 3.3 / Eq. recover_eqn: every FP32 operand entry a is split into an
+ *   FP16 high word hi = fl16(a) and an FP16 scaled residual
+ *   lo = fl16((a - hi) * s), fl16 = round to nearest even with gradual
+ *   underflow.  The product is rebuilt from three FP16 GEMMs accumulated in
+ *   FP32,
+ *       C ~= A_hi B_hi + (A_lo B_hi + A_hi B_lo) / s,
+ *   and the lo*lo term is dropped (bounded by Eq. ll_bound).
+ *   Sec. 4.5: the three terms are accumulated either elementwise
+ *   (Eq. elementwise: one running FP32 accumulator, each k-block's three
+ *   products folded into it in turn) or termwise (Eq. termwise: three
+ *   separate FP32 accumulations, combined once at the end as
+ *   (HH + XA/s) + XB/s).
+ *
+ * Conventions shared by every entry point below:
+ *   - Matrices are ROW-MAJOR.  A is M x K with leading dimension lda >= K,
+ *     B is K x N with ldb >= N, C is M x N with ldc >= N (all counted in
+ *     elements).  Column-major callers pass the operands swapped
+ *     (C^T = B^T A^T).
+ *   - A, B, C (and the workspace) are DEVICE pointers owned by the caller,
+ *     who keeps them alive until the enqueued work completes.
+ *   - Every call is asynchronous: it validates its arguments on the host,
+ *     enqueues kernels on `stream` (a hipStream_t; 0 = the null stream) and
+ *     returns.  Argument errors are reported BEFORE any device work and leave
+ *     C untouched.  Device faults surface at the caller's next stream
+ *     synchronisation.
+ *   - No range guard: inputs with |a| >= 65520 (hi overflow) or with a scaled
+ *     residual >= 65520 (lo overflow, Rule 2 of Sec. 4.2 violated) produce
+ *     IEEE inf/NaN in the affected outputs, deterministically (Sec. 3.1 scope).
+ *     Entries below 2^-14 have a subnormal hi and lose the 22-bit guarantee of
+ *     Eq. split_error (Sec. 4.2); they are still computed as defined.
+ *   - Thread-safe; the library keeps no per-call state.
+ */
+#ifndef SGEMM_CUBE_H_
+#define SGEMM_CUBE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Accumulation orders (Sec. 4.5). */
+typedef enum {
+  SGEMM_CUBE_ELEMENTWISE = 0, /* Eq. elementwise */
+  SGEMM_CUBE_TERMWISE = 1     /* Eq. termwise */
+} sgemm_cube_order_t;
+
+/* Status codes returned by every entry point. */
+typedef enum {
+  SGEMM_CUBE_OK = 0,
+  SGEMM_CUBE_ERR_INVALID_VALUE = 1, /* bad dimension, stride, pointer, scale or order */
+  SGEMM_CUBE_ERR_NOT_SUPPORTED = 2, /* shape beyond the library's indexing limits */
+  SGEMM_CUBE_ERR_ALLOC = 3,         /* workspace could not be obtained */
+  SGEMM_CUBE_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
+} sgemm_cube_status_t;
+
+/*
+ * C = SGEMM-cube(A, B): FP32 in, FP32 out, C overwritten (no alpha/beta).
+ *
+ *   M, N, K      >= 0.  M == 0 or N == 0: nothing is done.  K == 0: C := +0.
+ *   A, lda       row-major M x K, lda >= max(1, K); non-NULL when M*K > 0.
+ *   B, ldb       row-major K x N, ldb >= max(1, N); non-NULL when K*N > 0.
+ *   C, ldc       row-major M x N, ldc >= max(1, N); non-NULL when M*N > 0;
+ *                must not overlap A or B.
+ *   scale        the residual scaling factor s = 2^{s_b} of Sec. 4.2: a finite
+ *                exact power of two in [1, 2^24].  Eq. sf_bounds gives the
+ *                valid range for an input's exponent window; 2^11 is the fixed
+ *                choice valid over the whole normal-FP16 range.  Any other
+ *                value -> SGEMM_CUBE_ERR_INVALID_VALUE.
+ *   accum_order  SGEMM_CUBE_ELEMENTWISE or SGEMM_CUBE_TERMWISE.
+ *   stream       HIP stream the work is enqueued on.
+ *
+ * Needs device workspace of sgemm_cube_workspace_size(M, N, K, accum_order)
+ * bytes, which this entry point takes stream-ordered from a library-owned
+ * memory pool (hipMallocFromPoolAsync / hipFreeAsync on `stream`); failure ->
+ * SGEMM_CUBE_ERR_ALLOC.  Use sgemm_cube_ws to pass your own workspace.
+ */
+int sgemm_cube(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+               int64_t ldb, float* C, int64_t ldc, float scale, int accum_order,
+               hipStream_t stream);
+
+/*
+ * Same as sgemm_cube, with caller-provided device workspace `ws` of
+ * `ws_bytes` bytes (>= sgemm_cube_workspace_size(...), 256-byte aligned).
+ * `ws` may be NULL only when the required size is 0.  The workspace must not
+ * overlap A, B or C; its contents on entry are irrelevant and on exit are
+ * unspecified.  Calls that share a workspace must be ordered on one stream.
+ */
+int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                  int64_t ldb, float* C, int64_t ldc, float scale, int accum_order, void* ws,
+                  size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Two-phase form of sgemm_cube_ws, for callers that reuse a split operand
+ * (for example a constant B) or time the two passes separately:
+ *   sgemm_cube_prepare  splits A and B (Sec. 3.3) into the workspace;
+ *   sgemm_cube_compute  runs the three-product MFMA GEMM and the FP32
+ *                       reconstruction (Eq. recover_eqn, Sec. 4.5) from it.
+ * sgemm_cube_ws(...) == prepare(...) followed by compute(...) on one stream.
+ * M, N, K, the operands, scale, ws and ws_bytes follow sgemm_cube_ws; compute
+ * must be called with the same M, N, K and scale as the prepare whose
+ * workspace it reads (the library cannot check this).  prepare with A == NULL
+ * (or B == NULL) leaves that operand's planes untouched, so one operand can
+ * be re-split while the other's planes are kept.
+ */
+int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                       const float* B, int64_t ldb, float scale, void* ws, size_t ws_bytes,
+                       hipStream_t stream);
+int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
+                       int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Device workspace in bytes that sgemm_cube_ws needs for this problem
+ * (0 for degenerate shapes); 0 also for invalid arguments. */
+size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order);
+
+/*
+ * The two-component split alone (Sec. 3.3, Eq. recover_eqn), exposed so the
+ * split can be checked bit for bit:
+ *   hi[i*ldh + j] = fl16(X[i*ldx + j])
+ *   lo[i*ldh + j] = fl16((X[i*ldx + j] - hi) * scale)
+ * for 0 <= i < rows, 0 <= j < cols, as IEEE binary16 bit patterns.
+ *   rows, cols >= 0; ldx >= max(1, cols); ldh >= max(1, cols);
+ *   X, hi, lo device pointers, non-NULL when rows*cols > 0; hi and lo must not
+ *   overlap each other or X.  scale as for sgemm_cube.
+ */
+int sgemm_cube_split(int64_t rows, int64_t cols, const float* X, int64_t ldx, uint16_t* hi,
+                     uint16_t* lo, int64_t ldh, float scale, hipStream_t stream);
+
+/*
+ * Native-FP16 baseline (the HGEMM the paper compares against in Sec. 6.2):
+ *   C = sum_k fl16(A[i,k]) fl16(B[k,j]), FP16 products accumulated in FP32,
+ * i.e. the high-high term of Eq. recover_eqn alone.  Arguments and workspace
+ * handling as for sgemm_cube.
+ */
+int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                     const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char* sgemm_cube_status_string(int status);
+
+/* Size in elements of the elementwise k-block the GPU folds into its running
+ * accumulator (the block g of Eq. elementwise). */
+int sgemm_cube_block_k(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SGEMM_CUBE_H_ */

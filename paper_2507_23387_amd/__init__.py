@@ -1,0 +1,27 @@
+"""FP32-accuracy GEMM from three FP16 MFMA products on MI355X (gfx950).
+
+Implements the SGEMM-cube method of arXiv 2507.23387: FP32 operands split into
+an FP16 high word and a scaled FP16 residual (Sec. 3.3), the product rebuilt
+from three FP16 GEMMs with FP32 accumulation (Eq. recover_eqn), in the
+elementwise or termwise order (Sec. 4.5).  All computation happens in the HIP
+kernels of ``libsgemmcube.so``; ``binding`` is the ctypes layer over its C-ABI
+(include/sgemm_cube.h).
+"""
+from .binding import (  # noqa: F401
+    ELEMENTWISE,
+    TERMWISE,
+    SgemmCubeError,
+    hgemm,
+    matmul,
+    sgemm_cube,
+    sgemm_cube_block_k,
+    sgemm_cube_compute,
+    sgemm_cube_hgemm,
+    sgemm_cube_prepare,
+    sgemm_cube_split,
+    sgemm_cube_status_string,
+    sgemm_cube_workspace_size,
+    sgemm_cube_ws,
+    split,
+    workspace,
+)

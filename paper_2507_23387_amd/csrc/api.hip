@@ -1,0 +1,291 @@
+// C-ABI of libsgemmcube: argument validation, workspace, dispatch.
+// The interface and its conventions are documented in include/sgemm_cube.h.
+#include <atomic>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+
+#include "internal.h"
+#include "sgemm_cube.h"
+
+namespace sgc {
+
+Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base) {
+  Planes p{};
+  p.Mp = round_up(M, kBM);
+  p.Np = round_up(N, kBN);
+  p.Kp = round_up(K, kBK);
+  const size_t a_bytes = static_cast<size_t>(round_up(p.Mp * p.Kp * 2, 256));
+  const size_t b_bytes = static_cast<size_t>(round_up(p.Np * p.Kp * 2, 256));
+  char* c = static_cast<char*>(base);
+  p.a_hi = reinterpret_cast<uint16_t*>(c);
+  p.a_lo = reinterpret_cast<uint16_t*>(c + a_bytes);
+  p.b_hi = reinterpret_cast<uint16_t*>(c + 2 * a_bytes);
+  p.b_lo = reinterpret_cast<uint16_t*>(c + 2 * a_bytes + b_bytes);
+  p.bytes = 2 * a_bytes + 2 * b_bytes;
+  return p;
+}
+
+namespace {
+
+// Largest dimension the kernels index with 32-bit tile arithmetic; also keeps
+// every grid dimension within its hardware limit.
+constexpr int64_t kMaxDim = (int64_t{1} << 30);
+
+bool valid_scale(float s) {
+  if (!std::isfinite(s) || s < 1.0f || s > 16777216.0f) return false;
+  int e = 0;
+  return std::frexp(s, &e) == 0.5f;  // exact power of two
+}
+
+// Bytes spanned by a rows x cols row-major matrix with leading dimension ld.
+uint64_t span_bytes(int64_t rows, int64_t cols, int64_t ld, uint64_t elem) {
+  if (rows <= 0 || cols <= 0) return 0;
+  return (static_cast<uint64_t>(rows - 1) * static_cast<uint64_t>(ld) +
+          static_cast<uint64_t>(cols)) * elem;
+}
+
+bool overlap(const void* p, uint64_t pn, const void* q, uint64_t qn) {
+  if (pn == 0 || qn == 0) return false;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p), b = reinterpret_cast<uintptr_t>(q);
+  return a < b + qn && b < a + pn;
+}
+
+// Grid limits: GEMM workgroups = tiles_m * tiles_n must fit an int, and the
+// transposing split of B uses grid.y = Np / 64 <= 65535.
+bool round_up_tiles_exceed(int64_t M, int64_t N) {
+  return (round_up(M, kBM) / kBM) * (round_up(N, kBN) / kBN) > INT32_MAX ||
+         round_up(N, kBN) / 64 > 65535;
+}
+
+// ld * rows must not overflow int64 when forming addresses.
+bool ld_ok(int64_t rows, int64_t ld) {
+  return rows <= 1 || ld <= INT64_MAX / 8 / rows;
+}
+
+int validate_gemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                  int64_t ldb, const float* C, int64_t ldc, float scale, bool check_scale) {
+  if (M < 0 || N < 0 || K < 0) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (lda < (K > 1 ? K : 1) || ldb < (N > 1 ? N : 1) || ldc < (N > 1 ? N : 1))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (check_scale && !valid_scale(scale)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if ((M > 0 && K > 0 && !A) || (K > 0 && N > 0 && !B) || (M > 0 && N > 0 && !C))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!ld_ok(M, lda) || !ld_ok(K, ldb) || !ld_ok(M, ldc)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const uint64_t cb = span_bytes(M, N, ldc, 4);
+  if (overlap(C, cb, A, span_bytes(M, K, lda, 4)) || overlap(C, cb, B, span_bytes(K, N, ldb, 4)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  return SGEMM_CUBE_OK;
+}
+
+size_t ws_size(int64_t M, int64_t N, int64_t K) {
+  if (M == 0 || N == 0 || K == 0) return 0;
+  return plan_planes(M, N, K, nullptr).bytes;
+}
+
+// Enqueue the whole computation; arguments already validated.
+int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+        int64_t ldb, float* C, int64_t ldc, float scale, int variant, void* ws,
+        hipStream_t stream) {
+  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
+  if (K == 0) return launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
+                                                                     : SGEMM_CUBE_ERR_HIP;
+  const Planes p = plan_planes(M, N, K, ws);
+  if (launch_split_rows(M, K, A, lda, p.a_hi, p.a_lo, p.Kp, p.Mp, p.Kp, scale, stream) !=
+      hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (launch_split_cols_transposed(K, N, B, ldb, p.b_hi, p.b_lo, p.Np, p.Kp, scale, stream) !=
+      hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (launch_gemm(p, M, N, C, ldc, 1.0f / scale, variant, stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  return SGEMM_CUBE_OK;
+}
+
+// Library-owned, per-device stream-ordered memory pool for the workspace of
+// the allocating entry points.  The release threshold is raised so memory
+// freed at the end of a call is reused by the next one instead of going back
+// to the driver at every synchronisation.
+constexpr int kMaxDevices = 64;
+std::mutex g_pool_mu;
+hipMemPool_t g_pools[kMaxDevices] = {};
+
+int get_pool(hipMemPool_t* out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return SGEMM_CUBE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_pool_mu);
+  if (!g_pools[dev]) {
+    hipMemPoolProps props;
+    std::memset(&props, 0, sizeof props);
+    props.allocType = hipMemAllocationTypePinned;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = dev;
+    hipMemPool_t pool = nullptr;
+    if (hipMemPoolCreate(&pool, &props) != hipSuccess) return SGEMM_CUBE_ERR_ALLOC;
+    uint64_t threshold = UINT64_MAX;
+    if (hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold) != hipSuccess) {
+      (void)hipMemPoolDestroy(pool);
+      return SGEMM_CUBE_ERR_ALLOC;
+    }
+    g_pools[dev] = pool;
+  }
+  *out = g_pools[dev];
+  return SGEMM_CUBE_OK;
+}
+
+int run_allocating(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                   int64_t ldb, float* C, int64_t ldc, float scale, int variant,
+                   hipStream_t stream) {
+  const size_t need = ws_size(M, N, K);
+  if (need == 0) return run(M, N, K, A, lda, B, ldb, C, ldc, scale, variant, nullptr, stream);
+  hipMemPool_t pool = nullptr;
+  int st = get_pool(&pool);
+  if (st != SGEMM_CUBE_OK) return st;
+  void* ws = nullptr;
+  if (hipMallocFromPoolAsync(&ws, need, pool, stream) != hipSuccess || !ws)
+    return SGEMM_CUBE_ERR_ALLOC;
+  st = run(M, N, K, A, lda, B, ldb, C, ldc, scale, variant, ws, stream);
+  if (hipFreeAsync(ws, stream) != hipSuccess && st == SGEMM_CUBE_OK) st = SGEMM_CUBE_ERR_HIP;
+  return st;
+}
+
+}  // namespace
+}  // namespace sgc
+
+#pragma GCC visibility push(default)
+extern "C" {
+
+int sgemm_cube(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+               int64_t ldb, float* C, int64_t ldc, float scale, int accum_order,
+               hipStream_t stream) {
+  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
+  if (st != SGEMM_CUBE_OK) return st;
+  return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, stream);
+}
+
+int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                  int64_t ldb, float* C, int64_t ldc, float scale, int accum_order, void* ws,
+                  size_t ws_bytes, hipStream_t stream) {
+  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
+  if (st != SGEMM_CUBE_OK) return st;
+  const size_t need = sgc::ws_size(M, N, K);
+  if (ws_bytes < need || (need > 0 && (!ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (need > 0) {
+    if (sgc::overlap(ws, need, A, sgc::span_bytes(M, K, lda, 4)) ||
+        sgc::overlap(ws, need, B, sgc::span_bytes(K, N, ldb, 4)) ||
+        sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
+      return SGEMM_CUBE_ERR_INVALID_VALUE;
+  }
+  return sgc::run(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, ws, stream);
+}
+
+int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                       const float* B, int64_t ldb, float scale, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (lda < (K > 1 ? K : 1) || ldb < (N > 1 ? N : 1) || !sgc::valid_scale(scale))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::ld_ok(M, lda) || !sgc::ld_ok(K, ldb)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  const size_t need = sgc::ws_size(M, N, K);
+  if (need == 0) return SGEMM_CUBE_OK;
+  if (ws_bytes < need || !ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (sgc::overlap(ws, need, A, sgc::span_bytes(M, K, lda, 4)) ||
+      sgc::overlap(ws, need, B, sgc::span_bytes(K, N, ldb, 4)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  const sgc::Planes p = sgc::plan_planes(M, N, K, ws);
+  if (A && sgc::launch_split_rows(M, K, A, lda, p.a_hi, p.a_lo, p.Kp, p.Mp, p.Kp, scale,
+                                  stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (B && sgc::launch_split_cols_transposed(K, N, B, ldb, p.b_hi, p.b_lo, p.Np, p.Kp, scale,
+                                             stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  return SGEMM_CUBE_OK;
+}
+
+int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
+                       int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !sgc::valid_scale(scale))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
+  if (!C || !sgc::ld_ok(M, ldc)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (K == 0)
+    return sgc::launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
+                                                                : SGEMM_CUBE_ERR_HIP;
+  const size_t need = sgc::ws_size(M, N, K);
+  if (ws_bytes < need || !ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const sgc::Planes p = sgc::plan_planes(M, N, K, const_cast<void*>(ws));
+  return sgc::launch_gemm(p, M, N, C, ldc, 1.0f / scale, accum_order, stream) == hipSuccess
+             ? SGEMM_CUBE_OK
+             : SGEMM_CUBE_ERR_HIP;
+}
+
+size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order) {
+  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE) return 0;
+  if (M < 0 || N < 0 || K < 0 || M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim)
+    return 0;
+  return sgc::ws_size(M, N, K);
+}
+
+int sgemm_cube_split(int64_t rows, int64_t cols, const float* X, int64_t ldx, uint16_t* hi,
+                     uint16_t* lo, int64_t ldh, float scale, hipStream_t stream) {
+  if (rows < 0 || cols < 0) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (ldx < (cols > 1 ? cols : 1) || ldh < (cols > 1 ? cols : 1))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::valid_scale(scale)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (rows == 0 || cols == 0) return SGEMM_CUBE_OK;
+  if (!X || !hi || !lo) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::ld_ok(rows, ldx) || !sgc::ld_ok(rows, ldh)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const uint64_t xb = sgc::span_bytes(rows, cols, ldx, 4);
+  const uint64_t hb = sgc::span_bytes(rows, cols, ldh, 2);
+  if (sgc::overlap(hi, hb, lo, hb) || sgc::overlap(hi, hb, X, xb) || sgc::overlap(lo, hb, X, xb))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (cols > (int64_t{1} << 40)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  return sgc::launch_split_rows(rows, cols, X, ldx, hi, lo, ldh, rows, cols, scale, stream) ==
+                 hipSuccess
+             ? SGEMM_CUBE_OK
+             : SGEMM_CUBE_ERR_HIP;
+}
+
+int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                     const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream) {
+  const int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, 1.0f, false);
+  if (st != SGEMM_CUBE_OK) return st;
+  // The hi-only baseline uses the residual planes of the workspace for nothing;
+  // the split still fills them so the whole split pass is shared.
+  return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, 1.0f, sgc::kHiOnly, stream);
+}
+
+const char* sgemm_cube_status_string(int status) {
+  switch (status) {
+    case SGEMM_CUBE_OK: return "SGEMM_CUBE_OK";
+    case SGEMM_CUBE_ERR_INVALID_VALUE: return "SGEMM_CUBE_ERR_INVALID_VALUE";
+    case SGEMM_CUBE_ERR_NOT_SUPPORTED: return "SGEMM_CUBE_ERR_NOT_SUPPORTED";
+    case SGEMM_CUBE_ERR_ALLOC: return "SGEMM_CUBE_ERR_ALLOC";
+    case SGEMM_CUBE_ERR_HIP: return "SGEMM_CUBE_ERR_HIP";
+    default: return "SGEMM_CUBE_UNKNOWN_STATUS";
+  }
+}
+
+int sgemm_cube_block_k(void) { return sgc::kBK; }
+
+}  // extern "C"
+#pragma GCC visibility pop

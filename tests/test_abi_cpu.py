@@ -1,0 +1,143 @@
+"""Host-side checks of the C-ABI (no GPU needed): the library loads, exports
+every entry point include/sgemm_cube.h declares, and rejects invalid arguments
+before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sgemm_cube.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2507_23387_amd import binding
+
+    return binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sgemm_cube\w*)\s*\(", text)))
+
+
+def test_header_declares_expected_entry_points(lib):
+    assert declared_functions() == sorted(lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    raw = ctypes.CDLL(lib.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(raw, name), name
+
+
+def test_internal_symbols_hidden(lib):
+    raw = ctypes.CDLL(lib.LIB_PATH)
+    assert not hasattr(raw, "_ZN3sgc11plan_planesElllPv")
+
+
+def test_status_strings(lib):
+    for code, name in lib.STATUS_NAMES.items():
+        assert lib.sgemm_cube_status_string(code) == name
+    assert lib.sgemm_cube_status_string(99) == "SGEMM_CUBE_UNKNOWN_STATUS"
+
+
+def test_block_k(lib):
+    assert lib.sgemm_cube_block_k() == 64
+
+
+def test_workspace_size(lib):
+    # four FP16 planes, padded to the 128 x 128 x 64 tiles
+    assert lib.sgemm_cube_workspace_size(8192, 8192, 8192) == 4 * 8192 * 8192 * 2
+    assert lib.sgemm_cube_workspace_size(1, 1, 1) == 2 * (128 * 64 * 2) * 2
+    assert lib.sgemm_cube_workspace_size(0, 5, 5) == 0
+    assert lib.sgemm_cube_workspace_size(5, 5, 0) == 0
+    assert lib.sgemm_cube_workspace_size(-1, 5, 5) == 0
+    assert lib.sgemm_cube_workspace_size(5, 5, 5, 7) == 0
+
+
+FAKE = 1 << 40  # a non-null address that is never dereferenced
+INVALID = 1
+NOT_SUPPORTED = 2
+
+
+def call(lib, M=4, N=4, K=4, A=FAKE, lda=None, B=FAKE + (1 << 30), ldb=None,
+         C=FAKE + (2 << 30), ldc=None, scale=2048.0, order=0):
+    lda = K if lda is None else lda
+    ldb = N if ldb is None else ldb
+    ldc = N if ldc is None else ldc
+    return lib.sgemm_cube(M, N, K, A, lda, B, ldb, C, ldc, scale, order, 0)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(M=-1), dict(N=-1), dict(K=-1),
+    dict(lda=3), dict(ldb=3), dict(ldc=3),
+    dict(A=0), dict(B=0), dict(C=0),
+    dict(scale=3.0), dict(scale=0.5), dict(scale=2.0**25), dict(scale=float("inf")),
+    dict(scale=float("nan")), dict(scale=-2048.0), dict(scale=0.0),
+    dict(order=2), dict(order=-1),
+    dict(C=FAKE + 8),                        # C overlaps A
+    dict(C=FAKE + (1 << 30) + 4),            # C overlaps B
+])
+def test_invalid_arguments_rejected_before_device_work(lib, kw):
+    assert call(lib, **kw) == INVALID
+
+
+def test_too_large_is_not_supported(lib):
+    assert call(lib, M=(1 << 30) + 1, K=4, B=1 << 44, C=1 << 45) == NOT_SUPPORTED
+
+
+def test_valid_scales_accepted_by_validation(lib):
+    # Only validation is exercised here: M = 0 makes the call a no-op that
+    # returns before any device work.
+    for s_b in (0, 1, 11, 12, 13, 24):
+        assert call(lib, M=0, scale=2.0**s_b) == 0
+
+
+def test_degenerate_shapes_are_noops(lib):
+    assert call(lib, M=0) == 0
+    assert call(lib, N=0, ldb=1, ldc=1) == 0
+    assert call(lib, M=0, A=0, C=0) == 0        # null allowed when the extent is empty
+
+
+def test_ws_requires_workspace(lib):
+    need = lib.sgemm_cube_workspace_size(4, 4, 4)
+    ws = FAKE + (3 << 30)
+    args = (4, 4, 4, FAKE, 4, FAKE + (1 << 30), 4, FAKE + (2 << 30), 4, 2048.0, 0)
+    assert lib.sgemm_cube_ws(*args, 0, need, 0) == INVALID           # null ws
+    assert lib.sgemm_cube_ws(*args, ws, need - 1, 0) == INVALID      # too small
+    assert lib.sgemm_cube_ws(*args, ws + 16, need, 0) == INVALID     # misaligned
+    assert lib.sgemm_cube_ws(*args, FAKE, need, 0) == INVALID        # overlaps A
+
+
+def test_split_validation(lib):
+    X, H, L = FAKE, FAKE + (1 << 30), FAKE + (2 << 30)
+    assert lib.sgemm_cube_split(-1, 4, X, 4, H, L, 4, 2048.0, 0) == INVALID
+    assert lib.sgemm_cube_split(4, 4, X, 3, H, L, 4, 2048.0, 0) == INVALID
+    assert lib.sgemm_cube_split(4, 4, X, 4, H, L, 3, 2048.0, 0) == INVALID
+    assert lib.sgemm_cube_split(4, 4, X, 4, H, H + 4, 4, 2048.0, 0) == INVALID
+    assert lib.sgemm_cube_split(4, 4, X, 4, H, L, 4, 6.0, 0) == INVALID
+    assert lib.sgemm_cube_split(4, 4, 0, 4, H, L, 4, 2048.0, 0) == INVALID
+    assert lib.sgemm_cube_split(0, 4, 0, 4, 0, 0, 4, 2048.0, 0) == 0
+
+
+def test_prepare_compute_validation(lib):
+    need = lib.sgemm_cube_workspace_size(4, 4, 4)
+    ws = FAKE + (3 << 30)
+    assert lib.sgemm_cube_prepare(4, 4, 4, FAKE, 4, FAKE + (1 << 30), 4, 3.0, ws, need, 0) == INVALID
+    assert lib.sgemm_cube_prepare(4, 4, 4, FAKE, 4, FAKE + (1 << 30), 4, 2048.0, ws, need - 1,
+                                  0) == INVALID
+    assert lib.sgemm_cube_compute(4, 4, 4, FAKE, 4, 2048.0, 5, ws, need, 0) == INVALID
+    assert lib.sgemm_cube_compute(4, 4, 4, FAKE, 4, 2048.0, 0, 0, need, 0) == INVALID
+    assert lib.sgemm_cube_compute(4, 4, 4, ws + 64, 4, 2048.0, 0, ws, need, 0) == INVALID
+    assert lib.sgemm_cube_compute(0, 4, 4, 0, 4, 2048.0, 0, 0, 0, 0) == 0
+
+
+def test_hgemm_validation(lib):
+    assert lib.sgemm_cube_hgemm(4, 4, 4, FAKE, 3, FAKE + (1 << 30), 4, FAKE + (2 << 30), 4,
+                                0) == INVALID
+    assert lib.sgemm_cube_hgemm(0, 4, 4, FAKE, 4, FAKE + (1 << 30), 4, FAKE + (2 << 30), 4,
+                                0) == 0

@@ -1,0 +1,224 @@
+"""GPU GEMM (sgemm_cube, sgemm_cube_hgemm) against the oracle.
+
+Bar: |C_gpu - C_oracle|_ij <= 2 K 2^-24 (|A||B|)_ij for every compared entry,
+equality where (|A||B|)_ij = 0, identical inf/NaN patterns.  The oracle runs
+with the GPU's elementwise block size (sgemm_cube_block_k() = 64), so both
+sides fold the same blocks g of Eq. elementwise; only the summation order
+inside a block differs (MFMA versus sequential).
+
+Small and ragged shapes are compared in full; the five workloads at their full
+size are compared on sampled rows (each output row needs only its row of A
+and all of B, so the oracle computes exactly those rows)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from oracle import bounds
+from tests.gpu_util import gemm, hgemm, log, padded, to_dev
+from tests.helpers import abs_ab, assert_parity, ref64
+
+pytestmark = pytest.mark.gpu
+
+ORDERS = ["elementwise", "termwise"]
+SHAPES = [
+    (1, 1, 1), (1, 7, 3), (5, 3, 1), (17, 33, 65), (64, 64, 64), (128, 128, 64),
+    (129, 130, 65), (300, 200, 1000), (256, 256, 256), (200, 129, 4103), (513, 640, 192),
+]
+
+
+def _kb():
+    from paper_2507_23387_amd import binding
+
+    return binding.sgemm_cube_block_k()
+
+
+@pytest.mark.parametrize("order", ORDERS)
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_shapes_full_parity(gpu, order, shape):
+    M, N, K = shape
+    log(f"gemm {order} {M}x{N}x{K}")
+    A, B = workloads.make_operands(M, N, K, M + N + K, "normal")
+    C = gemm(A, B, 2048.0, order)
+    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb())
+    assert_parity(C, Co, K, abs_ab(A, B), f"{order} {shape}")
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1), (129, 130, 65), (256, 256, 256), (300, 200, 1000)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_hgemm_parity(gpu, shape):
+    M, N, K = shape
+    log(f"hgemm {M}x{N}x{K}")
+    A, B = workloads.make_operands(M, N, K, 77, "uniform_pm1")
+    C = hgemm(A, B)
+    Co = oracle.sgemm(A, B, 2048.0, "hi_only", kb=_kb())
+    assert_parity(C, Co, K, abs_ab(A, B), "hgemm")
+
+
+@pytest.mark.parametrize("order", ORDERS)
+def test_padded_leading_dimensions_and_misaligned_bases(gpu, order):
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K = 133, 71, 300
+    lda, ldb, ldc = K + 3, N + 5, N + 7
+    log(f"gemm padded ld {order}")
+    A, B = workloads.make_operands(M, N, K, 5, "uniform_pm1")
+    _, Av = padded(A, lda, offset=1)
+    _, Bv = padded(B, ldb, offset=3)
+    Cbuf = torch.full((2 + M * ldc,), float("nan"), dtype=torch.float32, device="cuda")
+    Cv = Cbuf[2:].view(M, ldc)
+    st = binding.sgemm_cube(M, N, K, Av.data_ptr(), lda, Bv.data_ptr(), ldb, Cv.data_ptr(), ldc,
+                            2048.0, binding.ORDERS[order], torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    Cn = Cv.cpu().numpy()
+    assert np.isnan(Cn[:, N:]).all(), "wrote outside the M x N block"
+    assert np.isnan(Cbuf[:2].cpu().numpy()).all()
+    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb())
+    assert_parity(Cn[:, :N], Co, K, abs_ab(A, B), "padded")
+
+
+def test_k_zero_writes_zero_and_empty_is_noop(gpu):
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    log("gemm K=0 / M=0")
+    C = torch.full((5, 6), float("nan"), device="cuda")
+    A = torch.empty((5, 0), device="cuda")
+    B = torch.empty((0, 6), device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    assert binding.sgemm_cube(5, 6, 0, A.data_ptr(), 1, B.data_ptr(), 6, C.data_ptr(), 6, 2048.0,
+                              0, stream) == 0
+    torch.cuda.synchronize()
+    assert (C.cpu().numpy() == 0).all()
+    C.fill_(float("nan"))
+    assert binding.sgemm_cube(0, 6, 4, 0, 4, B.data_ptr(), 6, C.data_ptr(), 6, 2048.0, 1,
+                              stream) == 0
+    torch.cuda.synchronize()
+    assert np.isnan(C.cpu().numpy()).all()
+
+
+@pytest.mark.parametrize("order", ORDERS)
+def test_non_finite_inputs_propagate_like_the_oracle(gpu, order):
+    """No range guard (Sec. 3.1): |a| >= 65520, lo overflow, inf and NaN
+    inputs give the same inf/NaN pattern as the oracle."""
+    M, N, K = 40, 50, 70
+    A, B = workloads.make_operands(M, N, K, 9, "uniform_pm1")
+    A[3, 5] = 70000.0      # hi overflows
+    A[7, 9] = np.inf
+    B[11, 13] = np.nan
+    B[20, 21] = 32784.0    # lo overflows with s = 2^12 (Sec. 4.2 example)
+    log(f"gemm non-finite {order}")
+    C = gemm(A, B, 4096.0, order)
+    Co = oracle.sgemm(A, B, 4096.0, order, kb=_kb())
+    assert_parity(C, Co, K, abs_ab(A, B), "non-finite")
+    assert np.isnan(Co).any()
+
+
+def test_subnormal_fp16_products_exact(gpu):
+    """FP16-subnormal operands (the 2^-14-scaled workload's regime): with
+    exactly representable FP16 inputs whose products and sums are exact in
+    FP32, the hi-only GEMM must be exact -- the MFMA must neither flush FP16
+    denormal inputs nor lose bits of the exact products."""
+    rng = np.random.default_rng(4)
+    M, N, K = 64, 48, 96
+    A = (rng.integers(-1023, 1024, size=(M, K)) * 2.0**-24).astype(np.float32)   # subnormal
+    B = rng.integers(-8, 9, size=(K, N)).astype(np.float32)
+    log("hgemm subnormal exact")
+    C = hgemm(A, B)
+    assert np.array_equal(C.astype(np.float64), ref64(A, B))
+    log("sgemm subnormal exact")
+    C2 = gemm(A, B, 2048.0, "termwise")
+    assert np.array_equal(C2.astype(np.float64), ref64(A, B))
+
+
+def test_deterministic_and_entry_points_agree(gpu):
+    """Repeated calls are bitwise identical, and sgemm_cube (pool workspace),
+    sgemm_cube_ws and prepare + compute compute the same bits."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K = 300, 257, 515
+    A, B = workloads.make_operands(M, N, K, 12, "normal")
+    dA, dB = to_dev(A), to_dev(B)
+    stream = torch.cuda.current_stream().cuda_stream
+    for order in ORDERS:
+        log(f"entry points agree {order}")
+        C1 = binding.matmul(dA, dB, 2048.0, order)
+        C2 = binding.matmul(dA, dB, 2048.0, order)
+        ws = binding.workspace(M, N, K)
+        C3 = binding.matmul(dA, dB, 2048.0, order, workspace=ws)
+        C4 = torch.empty_like(C1)
+        nbytes = ws.numel()
+        assert binding.sgemm_cube_prepare(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, 2048.0,
+                                          ws.data_ptr(), nbytes, stream) == 0
+        assert binding.sgemm_cube_compute(M, N, K, C4.data_ptr(), N, 2048.0,
+                                          binding.ORDERS[order], ws.data_ptr(), nbytes,
+                                          stream) == 0
+        torch.cuda.synchronize()
+        for X in (C2, C3, C4):
+            assert torch.equal(C1, X)
+
+
+def test_side_stream(gpu):
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K = 257, 300, 129
+    A, B = workloads.make_operands(M, N, K, 13, "uniform_pm1")
+    dA, dB = to_dev(A), to_dev(B)
+    log("gemm on a side stream")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        C = binding.matmul(dA, dB, 2048.0, "termwise")
+    s.synchronize()
+    Co = oracle.sgemm(A, B, 2048.0, "termwise", kb=_kb())
+    assert_parity(C.cpu().numpy(), Co, K, abs_ab(A, B), "side stream")
+
+
+# --- the five workloads at full size, sampled rows ----------------------------
+
+CASES = [
+    ("c1", "elementwise", 2.0**11), ("c1", "termwise", 2.0**11),
+    ("c2", "elementwise", 2.0**11), ("c2", "termwise", 2.0**11),
+    ("c3", "elementwise", 2.0**11),
+    ("c4", "elementwise", 2.0**11), ("c4", "termwise", 2.0**11),
+    ("c5", "termwise", 2.0**11), ("c5", "termwise", 2.0**13),
+    ("c5", "elementwise", 2.0**11), ("c5", "elementwise", 2.0**13),
+]
+_CACHE = {}
+
+
+def _operands(name):
+    if name not in _CACHE:
+        _CACHE.clear()
+        _CACHE[name] = workloads.workload_operands(name)
+    return _CACHE[name]
+
+
+@pytest.mark.parametrize("name,order,scale", CASES,
+                         ids=[f"{n}-{o}-{int(np.log2(s))}" for n, o, s in CASES])
+def test_workload_parity_sampled_rows(gpu, name, order, scale):
+    w = workloads.get(name)
+    A, B = _operands(name)
+    log(f"workload {w.name} {order} s=2^{int(np.log2(scale))}")
+    C = gemm(A, B, scale, order)
+    assert C.shape == (w.M, w.N)
+    rows = np.arange(w.M) if w.M <= 256 else workloads.sample_rows(w.M, 16, w.seed)
+    Co = oracle.sgemm_rows(A, B, rows, scale, order, kb=_kb())
+    absab = abs_ab(A, B, rows)
+    assert_parity(C[rows], Co, w.K, absab, f"{name} {order}")
+    # The whole output is finite (every workload stays in range).
+    assert np.isfinite(C).all()
+    # Termwise inside the exponent window of Rules 1-2 (all of the 4096^3
+    # normal and long-K workloads): Eq. main_bound against an FP64 GEMM.
+    if order == "termwise" and name in ("c2", "c4"):
+        coef = float(bounds.main_bound_coef(w.K))
+        err = np.abs(C[rows].astype(np.float64) - ref64(A, B, rows))
+        assert np.all(err <= coef * absab)
