@@ -37,6 +37,7 @@ namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTileHalves = kBM * kBK;  // halves per plane tile per stage
 
@@ -62,6 +63,41 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& 
   tn = in_group / gsize;
 }
 
+// Global -> registers: the 128 x 64 k-tile kt of each plane, 16 B per chunk,
+// 4 chunks per thread per plane (chunk c: row c / 8, k-chunk c % 8).
+template <int NP>
+__device__ __forceinline__ void global_load(const uint16_t* const (&src)[4], int Kp, int kt,
+                                            int t, u32x4 (&stg)[NP][4]) {
+  const int k0 = kt * kBK;
+#pragma unroll
+  for (int p = 0; p < NP; ++p)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = i * kThreads + t;
+      const int row = c >> 3;
+      const int kc = c & 7;
+      stg[p][i] = *reinterpret_cast<const u32x4*>(src[p] + static_cast<size_t>(row) * Kp + k0 +
+                                                  kc * 8);
+    }
+}
+
+// Registers -> LDS stage, 16-byte chunks XOR-swizzled by (row & 7).
+template <int NP>
+__device__ __forceinline__ void lds_store(uint16_t* lds, int stage, int t,
+                                          const u32x4 (&stg)[NP][4]) {
+  uint16_t* base = lds + stage * NP * kTileHalves;
+#pragma unroll
+  for (int p = 0; p < NP; ++p)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = i * kThreads + t;
+      const int row = c >> 3;
+      const int kc = c & 7;
+      *reinterpret_cast<u32x4*>(base + p * kTileHalves + row * kBK + ((kc ^ (row & 7)) << 3)) =
+          stg[p][i];
+    }
+}
+
 template <int V>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
@@ -80,37 +116,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(
 
   const size_t a_off = static_cast<size_t>(tm) * kBM * Kp;
   const size_t b_off = static_cast<size_t>(tn) * kBN * Kp;
-  const uint16_t* gsrc[4] = {a_hi + a_off, b_hi + b_off, (NP == 4) ? a_lo + a_off : nullptr,
+  const uint16_t* const gsrc[4] = {a_hi + a_off, b_hi + b_off, (NP == 4) ? a_lo + a_off : nullptr,
                              (NP == 4) ? b_lo + b_off : nullptr};
 
   // Staging registers: each plane tile is 1024 chunks of 16 B, 4 per thread.
-  uint4 stg[NP][4];
-  auto gload = [&](int kt) {
-    const int k0 = kt * kBK;
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = i * kThreads + t;
-        const int row = c >> 3;
-        const int kc = c & 7;
-        stg[p][i] = *reinterpret_cast<const uint4*>(gsrc[p] + static_cast<size_t>(row) * Kp +
-                                                    k0 + kc * 8);
-      }
-  };
-  auto lstore = [&](int stage) {
-    uint16_t* base = lds + stage * NP * kTileHalves;
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = i * kThreads + t;
-        const int row = c >> 3;
-        const int kc = c & 7;
-        *reinterpret_cast<uint4*>(base + p * kTileHalves + row * kBK + ((kc ^ (row & 7)) << 3)) =
-            stg[p][i];
-      }
-  };
+  u32x4 stg[NP][4];
 
   const floatx4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
   floatx4 acc[4][4];  // running accumulator (elementwise) or HH (termwise, hi-only)
@@ -122,15 +132,15 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(
     for (int j = 0; j < 4; ++j) acc[i][j] = xa[i][j] = xb[i][j] = zero;
 
   const int ktiles = Kp / kBK;
-  gload(0);
-  lstore(0);
+  global_load<NP>(gsrc, Kp, 0, t, stg);
+  lds_store<NP>(lds, 0, t, stg);
   __syncthreads();
 
   const int frag_row = lane & 15;          // row (A) / column (B) inside a 16 x 16 tile
   const int frag_kc = lane >> 4;           // which 8-wide k chunk of the 32-wide step
   for (int kt = 0; kt < ktiles; ++kt) {
     const bool more = kt + 1 < ktiles;
-    if (more) gload(kt + 1);
+    if (more) global_load<NP>(gsrc, Kp, kt + 1, t, stg);
     const uint16_t* s = lds + (kt & 1) * NP * kTileHalves;
 #pragma unroll
     for (int ks = 0; ks < kBK / 32; ++ks) {
@@ -175,7 +185,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(
             acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
           }
     }
-    if (more) lstore((kt + 1) & 1);
+    if (more) lds_store<NP>(lds, (kt + 1) & 1, t, stg);
     __syncthreads();
   }
 

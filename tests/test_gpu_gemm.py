@@ -95,7 +95,8 @@ def test_k_zero_writes_zero_and_empty_is_noop(gpu):
     torch.cuda.synchronize()
     assert (C.cpu().numpy() == 0).all()
     C.fill_(float("nan"))
-    assert binding.sgemm_cube(0, 6, 4, 0, 4, B.data_ptr(), 6, C.data_ptr(), 6, 2048.0, 1,
+    B4 = torch.ones((4, 6), device="cuda")
+    assert binding.sgemm_cube(0, 6, 4, 0, 4, B4.data_ptr(), 6, C.data_ptr(), 6, 2048.0, 1,
                               stream) == 0
     torch.cuda.synchronize()
     assert np.isnan(C.cpu().numpy()).all()
