@@ -15,7 +15,7 @@ Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base) {
   Planes p{};
   p.Mp = round_up(M, kBM);
   p.Np = round_up(N, kBN);
-  p.Kp = round_up(K, kBK);
+  p.Kp = round_up(K, kKPad);
   const size_t a_bytes = static_cast<size_t>(round_up(p.Mp * p.Kp * 2, 256));
   const size_t b_bytes = static_cast<size_t>(round_up(p.Np * p.Kp * 2, 256));
   char* c = static_cast<char*>(base);

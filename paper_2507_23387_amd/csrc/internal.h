@@ -15,10 +15,11 @@ enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2 };
 
 // GEMM tiling.  The split planes are padded to these multiples so the GEMM's
 // main loop needs no bounds checks; only the C store is masked.
-constexpr int kBM = 128;   // rows of C per workgroup
-constexpr int kBN = 128;   // columns of C per workgroup
-constexpr int kBK = 64;    // k per LDS stage; also the elementwise k-block
-constexpr int kThreads = 256;
+constexpr int kBM = 256;     // rows of C per workgroup
+constexpr int kBN = 128;     // columns of C per workgroup
+constexpr int kBK = 32;      // k per LDS stage; also the elementwise k-block
+constexpr int kKPad = 64;    // K is padded to a multiple of this (an even number of stages)
+constexpr int kThreads = 512;
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 

@@ -46,13 +46,13 @@ def test_status_strings(lib):
 
 
 def test_block_k(lib):
-    assert lib.sgemm_cube_block_k() == 64
+    assert lib.sgemm_cube_block_k() == 32
 
 
 def test_workspace_size(lib):
-    # four FP16 planes, padded to the 128 x 128 x 64 tiles
+    # four FP16 planes: A padded to 256-row tiles, B to 128-column tiles, K to 64
     assert lib.sgemm_cube_workspace_size(8192, 8192, 8192) == 4 * 8192 * 8192 * 2
-    assert lib.sgemm_cube_workspace_size(1, 1, 1) == 2 * (128 * 64 * 2) * 2
+    assert lib.sgemm_cube_workspace_size(1, 1, 1) == 2 * (256 * 64 * 2) + 2 * (128 * 64 * 2)
     assert lib.sgemm_cube_workspace_size(0, 5, 5) == 0
     assert lib.sgemm_cube_workspace_size(5, 5, 0) == 0
     assert lib.sgemm_cube_workspace_size(-1, 5, 5) == 0
