@@ -39,7 +39,9 @@ METRIC = "FP32-equiv TFLOP/s (2MNK/t) and % of 3-GEMM FP16 MFMA peak; max rel er
 FP16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12
 THREE_GEMM_PEAK_TFLOPS = FP16_PEAK_TFLOPS / 3
 HBM_PEAK_GBS = 8000.0
-GEMM_KERNEL = "gemm_kernel"
+# The MFMA kernel that runs for each order (the elementwise call also launches
+# the narrow kernel, which reads the range flag and returns at once).
+GEMM_KERNELS = {"elementwise": "gemm_wide_kernel<0>", "termwise": "gemm_narrow_kernel<1>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
@@ -219,7 +221,7 @@ def main():
     traffic = traffic_entry(w.name, order)
     roofline = {
         "bound": "mfma",
-        "kernel": f"{GEMM_KERNEL} ({order})",
+        "kernel": GEMM_KERNELS[order],
         "achieved": gemm_tflops,
         "peak": FP16_PEAK_TFLOPS,
         "unit": "TFLOP/s",

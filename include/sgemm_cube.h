@@ -146,8 +146,14 @@ int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t ld
 /* Static, human-readable name of a status code. */
 const char* sgemm_cube_status_string(int status);
 
-/* Size in elements of the elementwise k-block the GPU folds into its running
- * accumulator (the block g of Eq. elementwise). */
+/* Size in elements of the elementwise k-block g of Eq. elementwise on the
+ * main path (16, one MFMA k-step): there the running accumulator holds
+ * scale * acc and each block's three products are summed into it by the
+ * matrix unit in the order HH, XA, XB, each sum rounded once together with
+ * the accumulator.  When some |fl16(B)| * scale exceeds 65504 (scale * B_hi
+ * would overflow FP16) the elementwise order runs unscaled with blocks of
+ * twice this size instead: HH into the accumulator, XA_g and XB_g summed
+ * separately, acc = (acc + XA_g / s) + XB_g / s. */
 int sgemm_cube_block_k(void);
 
 #ifdef __cplusplus

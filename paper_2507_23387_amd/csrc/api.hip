@@ -13,17 +13,19 @@ namespace sgc {
 
 Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base) {
   Planes p{};
-  p.Mp = round_up(M, kBM);
-  p.Np = round_up(N, kBN);
+  p.Mp = round_up(M, kRowPad);
+  p.Np = round_up(N, kRowPad);
   p.Kp = round_up(K, kKPad);
   const size_t a_bytes = static_cast<size_t>(round_up(p.Mp * p.Kp * 2, 256));
   const size_t b_bytes = static_cast<size_t>(round_up(p.Np * p.Kp * 2, 256));
   char* c = static_cast<char*>(base);
+  p.range_flag = reinterpret_cast<int*>(c);
+  c += kFlagBytes;
   p.a_hi = reinterpret_cast<uint16_t*>(c);
   p.a_lo = reinterpret_cast<uint16_t*>(c + a_bytes);
   p.b_hi = reinterpret_cast<uint16_t*>(c + 2 * a_bytes);
   p.b_lo = reinterpret_cast<uint16_t*>(c + 2 * a_bytes + b_bytes);
-  p.bytes = 2 * a_bytes + 2 * b_bytes;
+  p.bytes = kFlagBytes + 2 * a_bytes + 2 * b_bytes;
   return p;
 }
 
@@ -52,11 +54,11 @@ bool overlap(const void* p, uint64_t pn, const void* q, uint64_t qn) {
   return a < b + qn && b < a + pn;
 }
 
-// Grid limits: GEMM workgroups = tiles_m * tiles_n must fit an int, and the
-// transposing split of B uses grid.y = Np / 64 <= 65535.
+// Grid limits: GEMM workgroups (at most (Mp / 256) * (Np / 128)) must fit an
+// int, and the split of B uses grid.y = Np / 128 <= 65535.
 bool round_up_tiles_exceed(int64_t M, int64_t N) {
-  return (round_up(M, kBM) / kBM) * (round_up(N, kBN) / kBN) > INT32_MAX ||
-         round_up(N, kBN) / 64 > 65535;
+  const int64_t Mp = round_up(M, kRowPad), Np = round_up(N, kRowPad);
+  return (Mp / 256) * (Np / 128) > INT32_MAX || Np / kPanel > 65535;
 }
 
 // ld * rows must not overflow int64 when forming addresses.
@@ -94,13 +96,9 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
   if (K == 0) return launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
                                                                      : SGEMM_CUBE_ERR_HIP;
   const Planes p = plan_planes(M, N, K, ws);
-  if (launch_split_rows(M, K, A, lda, p.a_hi, p.a_lo, p.Kp, p.Mp, p.Kp, scale, stream) !=
-      hipSuccess)
-    return SGEMM_CUBE_ERR_HIP;
-  if (launch_split_cols_transposed(K, N, B, ldb, p.b_hi, p.b_lo, p.Np, p.Kp, scale, stream) !=
-      hipSuccess)
-    return SGEMM_CUBE_ERR_HIP;
-  if (launch_gemm(p, M, N, C, ldc, 1.0f / scale, variant, stream) != hipSuccess)
+  if (launch_split_a(p, M, K, A, lda, scale, stream) != hipSuccess) return SGEMM_CUBE_ERR_HIP;
+  if (launch_split_b(p, K, N, B, ldb, scale, stream) != hipSuccess) return SGEMM_CUBE_ERR_HIP;
+  if (launch_gemm(p, M, N, C, ldc, scale, variant, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   return SGEMM_CUBE_OK;
 }
@@ -205,11 +203,9 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   const sgc::Planes p = sgc::plan_planes(M, N, K, ws);
-  if (A && sgc::launch_split_rows(M, K, A, lda, p.a_hi, p.a_lo, p.Kp, p.Mp, p.Kp, scale,
-                                  stream) != hipSuccess)
+  if (A && sgc::launch_split_a(p, M, K, A, lda, scale, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
-  if (B && sgc::launch_split_cols_transposed(K, N, B, ldb, p.b_hi, p.b_lo, p.Np, p.Kp, scale,
-                                             stream) != hipSuccess)
+  if (B && sgc::launch_split_b(p, K, N, B, ldb, scale, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   return SGEMM_CUBE_OK;
 }
@@ -233,7 +229,7 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
   if (sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   const sgc::Planes p = sgc::plan_planes(M, N, K, const_cast<void*>(ws));
-  return sgc::launch_gemm(p, M, N, C, ldc, 1.0f / scale, accum_order, stream) == hipSuccess
+  return sgc::launch_gemm(p, M, N, C, ldc, scale, accum_order, stream) == hipSuccess
              ? SGEMM_CUBE_OK
              : SGEMM_CUBE_ERR_HIP;
 }
@@ -259,7 +255,7 @@ int sgemm_cube_split(int64_t rows, int64_t cols, const float* X, int64_t ldx, ui
   if (sgc::overlap(hi, hb, lo, hb) || sgc::overlap(hi, hb, X, xb) || sgc::overlap(lo, hb, X, xb))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (cols > (int64_t{1} << 40)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
-  return sgc::launch_split_rows(rows, cols, X, ldx, hi, lo, ldh, rows, cols, scale, stream) ==
+  return sgc::launch_split_rows(rows, cols, X, ldx, hi, lo, ldh, scale, stream) ==
                  hipSuccess
              ? SGEMM_CUBE_OK
              : SGEMM_CUBE_ERR_HIP;
@@ -269,8 +265,8 @@ int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t ld
                      const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream) {
   const int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, 1.0f, false);
   if (st != SGEMM_CUBE_OK) return st;
-  // The hi-only baseline uses the residual planes of the workspace for nothing;
-  // the split still fills them so the whole split pass is shared.
+  // The hi-only baseline does not read the residual planes; the split still
+  // fills them so the whole split pass is shared.
   return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, 1.0f, sgc::kHiOnly, stream);
 }
 
@@ -285,7 +281,7 @@ const char* sgemm_cube_status_string(int status) {
   }
 }
 
-int sgemm_cube_block_k(void) { return sgc::kBK; }
+int sgemm_cube_block_k(void) { return sgc::kBlockScaled; }
 
 }  // extern "C"
 #pragma GCC visibility pop

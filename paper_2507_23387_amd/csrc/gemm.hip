@@ -1,40 +1,51 @@
 // Three-product MFMA GEMM on prepared FP16 planes (gfx950).
 //
-// For each 256 x 128 tile of C it computes (Eq. recover_eqn of arXiv
-// 2507.23387)
+// For each tile of C it forms (Eq. recover_eqn of arXiv 2507.23387)
 //   HH = A_hi B_hi,  XA = A_lo B_hi,  XB = A_hi B_lo
-// with v_mfma_f32_32x32x16_f16 (FP16 x FP16 products are exact; the MFMA sums
-// them with its C operand in one fused, once-rounded FP32 operation), and
-// reconstructs C in one of three ways:
-//   kElementwise (Eq. elementwise, Sec. 4.5): the contraction dimension is cut
-//     into blocks g of kBK = 32.  Per block the high-high products go straight
-//     into the running FP32 accumulator (its MFMA C operand -- the matrix-unit
-//     "C_blk <- A_blk B_blk + C_blk" of Alg. 1), the two cross products go into
-//     separate FP32 block sums started from zero, and at the end of the block
-//       acc = (acc + XA_g / s) + XB_g / s
-//     with two v_fma_f32 (1/s is an exact power of two, so each fma is exactly
-//     one rounded FP32 addition).
-//   kTermwise (Eq. termwise): three FP32 accumulators over all of K, combined
-//     once in the epilogue as C = (HH + XA / s) + XB / s.
+// with v_mfma_f32_32x32x16_f16 (FP16 x FP16 products are exact; the MFMA adds
+// the 16 products of a k-step to its C operand in one fused, once-rounded FP32
+// operation) and reconstructs C in the accumulation order asked for.
+//
+// Two kernels share one data path:
+//
+// gemm_wide_kernel, 256 x 256 tiles, 4 waves of 128 x 128 (one per SIMD, the
+// 256-register accumulator in AGPRs):
+//   kElementwise (Eq. elementwise, Sec. 4.5) with the contraction cut into
+//     blocks g of one k-step (16).  The accumulator holds s * acc, so that the
+//     three per-block additions of the equation become three chained MFMAs:
+//       s*acc <- fl(s*acc + A_hi (s B_hi))   = s * fl(acc + HH_g)
+//       s*acc <- fl(s*acc + A_lo B_hi)       = s * fl(acc + XA_g / s)
+//       s*acc <- fl(s*acc + A_hi B_lo)       = s * fl(acc + XB_g / s)
+//     and C = (s*acc) / s at the end.  s B_hi is formed in registers with
+//     v_pk_mul_f16; it is exact because s is a power of two, provided
+//     |B_hi| s <= 65504, which the split of B checks (the range flag).  Each
+//     block term is summed by the MFMA together with the accumulator, with
+//     one rounding, instead of being rounded to FP32 on its own first.
 //   kHiOnly: C = HH, the native-FP16 GEMM baseline.
 //
-// Data path.  A planes are Mp x Kp and B planes Np x Kp (B transposed), both
-// k-contiguous and zero-padded, so the main loop has no bounds checks.  Each
-// k-stage of 32 brings the workgroup's 256 + 128 rows x 32 k of every plane
-// (48 KiB) from global memory straight into LDS with global_load_lds_dwordx4
-// (no VGPR staging), into a ring of kStages stages, so the loads for stage
-// kt+2 are in flight while stage kt feeds the MFMAs (the double buffering of
-// Sec. 5.4 taken one step deeper).  Rows are 64 B; their four 16-byte chunks
-// are XOR-swizzled by (row >> 2) & 3 so that the MFMA fragment reads (16
-// consecutive rows at one chunk per LDS cycle) hit 16 distinct bank groups.
-// The loop body is branch-free (past the end it re-loads the last stage into
-// the free slot) so the vmcnt waits stay exact, and one s_barrier per stage
-// both publishes the landed stage and retires the stage being overwritten.
+// gemm_narrow_kernel, 256 x 128 tiles, 8 waves of 64 x 64 (two per SIMD):
+//   kTermwise (Eq. termwise): three FP32 accumulators over all of K,
+//     C = (HH + XA / s) + XB / s in the epilogue.
+//   kElementwise when the range flag is set: unscaled, blocks of two k-steps
+//     (32): HH goes straight into the accumulator, XA_g and XB_g into block
+//     sums started from zero, and acc = (acc + XA_g / s) + XB_g / s with two
+//     v_fma_f32 at the end of each block (1/s is exact).
+// Both elementwise kernels are launched; each reads the range flag first and
+// the one that does not apply returns at once.
 //
-// Workgroup: 512 threads = 8 waves (2 per SIMD) in a 4 x 2 grid; each wave owns
-// a 64 x 64 sub-tile = 2 x 2 MFMA tiles of 32 x 32, so 2 waves share each SIMD
-// and hide each other's LDS latency.  Accumulators: 64 (hi-only), 192
-// (termwise) or 64 + 128 block temporaries (elementwise) registers per lane.
+// Data path.  The planes are stored as 4 KiB tiles of 128 rows x 16 k in the
+// order and swizzle the LDS wants (internal.h), so one pipeline stage (one
+// k-step of every plane the kernel needs) is a few contiguous 4 KiB blocks,
+// copied from global memory straight into LDS with global_load_lds_dwordx4 (no
+// VGPR staging).  Stages go into a ring of kStages slots.  In k-step kt the
+// fragments of step kt+1 are read while the MFMAs of step kt run: each
+// fragment register is reloaded as soon as its last MFMA of the step has been
+// issued (a rolling schedule; it fits the register file where double
+// buffering does not), and the DMAs for stage kt+kStages are spread between
+// the MFMA groups so the in-order wave never stalls on a burst of memory
+// instructions.  One s_barrier per step both publishes stage kt+1 and retires
+// the slot of stage kt before it is refilled.  Past the last stage the loads
+// repeat the last stage, so every wait count is a compile-time constant.
 #include "internal.h"
 
 namespace sgc {
@@ -43,17 +54,9 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kWaves = kThreads / 64;  // 8
-constexpr int kWavesM = 4;
-constexpr int kWavesN = 2;
-constexpr int kWaveM = kBM / kWavesM;  // 64 rows per wave
-constexpr int kWaveN = kBN / kWavesN;  // 64 columns per wave
-constexpr int kSubM = kWaveM / 32;     // 2 MFMA tiles per wave along M
-constexpr int kSubN = kWaveN / 32;     // 2 along N
-constexpr int kStages = 3;
-constexpr int kChunksPerRow = kBK / 8;  // 16-byte chunks per LDS row (4)
-static_assert(kWavesM * kWavesN == kWaves, "wave grid");
-static_assert(kKPad % kBK == 0, "whole stages per padded K");
+constexpr int kKSteps = kSlice / 16;  // MFMA k-steps per tile slice (1)
+static_assert(kKSteps == 1, "one MFMA k-step per slice");
+static_assert(kKPad % (2 * kSlice) == 0, "the main loops take two slices per iteration");
 
 // D(32x32) = A(32x16) B(16x32) + C.  Lane l supplies A row l%32 and B column
 // l%32 with the 8 consecutive k values 8*(l/32) .. 8*(l/32)+7 of the 16-wide
@@ -62,14 +65,10 @@ __device__ __forceinline__ floatx16 mfma32(const half8& a, const half8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
-// Physical 16-byte chunk of logical chunk c in LDS row `row` (64-byte rows).
-__device__ __forceinline__ int swizzle(int row, int c) { return c ^ ((row >> 2) & 3); }
-
 // One 64-lane LDS DMA: lane l copies 16 bytes from g into LDS byte address
-// lds_addr + 16 * l.  Issued as inline asm so the compiler does not add its
-// own conservative vmcnt(0) waits before every later LDS read; the kernel
-// waits explicitly with wait_vmcnt<>() before the barrier that publishes a
-// stage.
+// lds_addr + 16 * l.  Inline asm, so the compiler adds no conservative vmcnt(0)
+// before later LDS reads; the kernels wait explicitly with wait_vmcnt<>()
+// before the barrier that publishes a stage.
 __device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
                : "memory", "m0");
@@ -85,15 +84,29 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Keeps the instruction groups of the schedule in program order.
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// Offset (halves) of the fragment of LDS row r for k chunk fk (0 or 1).
+__device__ __forceinline__ int frag_offset(int r, int fk) {
+  return r * kSlice + ((fk ^ tile_swizzle(r)) << 3);
+}
+
+// LDS byte address of the dynamic shared-memory base (the M0 operand of the
+// DMA): cast the generic pointer to the LDS address space, then to int.
+__device__ __forceinline__ unsigned lds_address(const uint16_t* p) {
+  return static_cast<unsigned>((uintptr_t)((__attribute__((address_space(3))) const uint16_t*)p));
+}
+
 // Map the hardware workgroup id to a (tile_m, tile_n) pair.  Workgroups are
 // dispatched round-robin over the 8 XCDs; renumbering gives each XCD a
-// contiguous range of logical tiles, and grouping 8 tile-rows keeps the A
+// contiguous range of logical tiles, and grouping kGroup tile-rows keeps the A
 // and B panels a group touches resident in that XCD's L2.
+template <int kGroup>
 __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nwg = tiles_m * tiles_n;
   int wg = blockIdx.x;
   if ((nwg & 7) == 0) wg = (wg & 7) * (nwg >> 3) + (wg >> 3);
-  constexpr int kGroup = 8;
   const int per_group = kGroup * tiles_n;
   const int group = wg / per_group;
   const int first_m = group * kGroup;
@@ -103,189 +116,429 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& 
   tn = in_group / gsize;
 }
 
+// Store a wave's accumulators: register r of MFMA tile (i, j) holds row
+// 8*(r/4) + 4*(l/32) + r%4 and column l%32 of that 32 x 32 tile.  `value`
+// maps (i, j, r) to the float to store.  Tiles entirely inside C take the
+// unmasked path; row offsets are wave-uniform multiples of ldc.
+template <int kSubM, int kSubN, typename F>
+__device__ __forceinline__ void store_tile(float* __restrict__ C, int64_t ldc, int M, int N,
+                                           int row0, int col0, bool full, F value) {
+  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
+  if (full) {
+#pragma unroll
+    for (int i = 0; i < kSubM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float* const p = base + static_cast<int64_t>(i * 32 + (r >> 2) * 8 + (r & 3)) * ldc;
+#pragma unroll
+        for (int j = 0; j < kSubN; ++j) p[j * 32] = value(i, j, r);
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kSubM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rr = i * 32 + (r >> 2) * 8 + (r & 3);
+        float* const p = base + static_cast<int64_t>(rr) * ldc;
+#pragma unroll
+        for (int j = 0; j < kSubN; ++j)
+          if (row0 + rr < M && col0 + j * 32 < N) p[j * 32] = value(i, j, r);
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 256 x 256 tiles: scaled elementwise and hi-only.
+constexpr int kWide = 256;
+constexpr int kWideThreads = 256;
+constexpr int kWideStages = 4;
+
 template <int V>
-__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(
+constexpr int wide_planes() { return V == kElementwise ? 4 : 2; }
+
+template <int V>
+constexpr size_t wide_lds_bytes() {
+  return static_cast<size_t>(kWideStages) * wide_planes<V>() * kWide * kSlice * 2;
+}
+
+template <int V>
+__global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
-    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo, int Kp, int tiles_m,
-    int tiles_n, float* __restrict__ C, int64_t ldc, int M, int N, float inv_s) {
-  // Planes staged per stage: A_hi, B_hi [, A_lo, B_lo].
-  constexpr int kPairs = (V == kHiOnly) ? 1 : 2;
-  constexpr int kABlocks = kBM * kChunksPerRow / 64;  // 64-chunk DMA blocks per A plane tile
-  constexpr int kBBlocks = kBN * kChunksPerRow / 64;
-  static_assert(kABlocks % kWaves == 0 && kBBlocks % kWaves == 0, "DMA blocks per wave");
-  constexpr int kDmaPerStage = kPairs * (kABlocks + kBBlocks) / kWaves;  // per wave
-  constexpr int kAPlane = kBM * kBK;  // halves
-  constexpr int kBPlane = kBN * kBK;
-  constexpr int kStage = kPairs * (kAPlane + kBPlane);
-  constexpr int kOffAH = 0, kOffBH = kAPlane, kOffAL = kAPlane + kBPlane,
-                kOffBL = 2 * kAPlane + kBPlane;
-  constexpr int kSteps = kBK / 16;  // MFMA k-steps per stage
+    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
+    const int* __restrict__ range_flag, int Kp, int tiles_m, int tiles_n,
+    float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
+  static_assert(V == kElementwise || V == kHiOnly, "wide kernel variants");
+  constexpr bool kEl = V == kElementwise;
+  constexpr int S = kWideStages;
+  constexpr int kPlanes = wide_planes<V>();       // LDS slots: A_hi, B_hi, A_lo, B_lo
+  constexpr int kPlaneHalves = kWide * kSlice;    // two tiles
+  constexpr int kStageHalves = kPlanes * kPlaneHalves;
+  constexpr int kDma = kPlanes * 2;               // 1 KiB DMAs per wave per stage
+  constexpr int kSub = 4;                         // 32 x 32 MFMA tiles per wave side
+  if constexpr (kEl) {
+    if (*range_flag) return;  // |B_hi| s overflows FP16: the narrow kernel runs instead
+  }
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
-  tile_of(tiles_m, tiles_n, tm, tn);
+  tile_of<4>(tiles_m, tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = wave / kWavesN;
-  const int wn = wave % kWavesN;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  const int64_t slices = Kp / kSlice;
+  const int ktiles = static_cast<int>(slices);
 
-  const uint16_t* const ga[2] = {a_hi + static_cast<size_t>(tm) * kBM * Kp,
-                                 a_lo + static_cast<size_t>(tm) * kBM * Kp};
-  const uint16_t* const gb[2] = {b_hi + static_cast<size_t>(tn) * kBN * Kp,
-                                 b_lo + static_cast<size_t>(tn) * kBN * Kp};
-  // LDS byte address of the dynamic shared-memory base (the M0 operand of the
-  // DMA): cast the generic pointer to the LDS address space, then to int.
-  const unsigned lds_base = static_cast<unsigned>(
-      (uintptr_t)((__attribute__((address_space(3))) uint16_t*)lds));
-
-  // DMA the k-stage kt into ring slot `slot`.  LDS slot q of a plane tile holds
-  // logical chunk swizzle(row, q % 4) of row q / 4; lane l of DMA block b
-  // fills slot 64 b + l, so each instruction writes 1 KiB contiguously.
-  auto issue = [&](int kt, int slot) {
-    const unsigned base = lds_base + slot * kStage * 2;
-    const int k0 = kt * kBK;
-#pragma unroll
-    for (int p = 0; p < kPairs; ++p) {
-#pragma unroll
-      for (int i = 0; i < kABlocks / kWaves; ++i) {
-        const int blk = i * kWaves + wave;
-        const int q = blk * 64 + lane;
-        const int row = q / kChunksPerRow;
-        const int c = swizzle(row, q % kChunksPerRow);
-        dma16(ga[p] + static_cast<size_t>(row) * Kp + k0 + c * 8,
-              base + ((p ? kOffAL : kOffAH) + blk * 512) * 2);
-      }
-#pragma unroll
-      for (int i = 0; i < kBBlocks / kWaves; ++i) {
-        const int blk = i * kWaves + wave;
-        const int q = blk * 64 + lane;
-        const int row = q / kChunksPerRow;
-        const int c = swizzle(row, q % kChunksPerRow);
-        dma16(gb[p] + static_cast<size_t>(row) * Kp + k0 + c * 8,
-              base + ((p ? kOffBL : kOffBH) + blk * 512) * 2);
-      }
-    }
+  // Wave w copies 1 KiB block w of both tiles (panel 2t and 2t+1) of each
+  // plane per stage: 32 rows of 16 k.
+  const int64_t panel_stride = slices * kTileHalves;
+  const uint16_t* src[4] = {a_hi + 2 * tm * panel_stride, b_hi + 2 * tn * panel_stride,
+                            kEl ? a_lo + 2 * tm * panel_stride : nullptr,
+                            kEl ? b_lo + 2 * tn * panel_stride : nullptr};
+  const int64_t lane_off = w * 512 + lane * 8;
+  const unsigned lds_base = lds_address(lds);
+  auto dma_one = [&](int kt, int n) {  // n-th DMA of stage kt, n < kDma
+    const int ktc = min(kt, ktiles - 1);
+    const int p = n >> 1, half = n & 1;
+    const unsigned dst = lds_base + ((kt % S) * kStageHalves + p * kPlaneHalves +
+                                     (half * 4 + w) * 512) * 2;
+    dma16(src[p] + half * panel_stride + static_cast<int64_t>(ktc) * kTileHalves + lane_off, dst);
   };
 
-  const floatx16 zero = {};
-  floatx16 acc[kSubM][kSubN];  // running accumulator (elementwise) or HH
-  floatx16 xa[kSubM][kSubN];   // termwise XA, or elementwise block sum XA_g
-  floatx16 xb[kSubM][kSubN];   // termwise XB, or elementwise block sum XB_g
+  const int fr = lane & 31, fk = lane >> 5;
+  int aoff[kSub], boff[kSub];
 #pragma unroll
-  for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-    for (int j = 0; j < kSubN; ++j) acc[i][j] = xa[i][j] = xb[i][j] = zero;
+  for (int i = 0; i < kSub; ++i) {
+    aoff[i] = frag_offset(wm * 128 + i * 32 + fr, fk);
+    boff[i] = frag_offset(wn * 128 + i * 32 + fr, fk);
+  }
+  auto rd = [&](int kt, int slot, int off) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + slot * kPlaneHalves +
+                                           off);
+  };
+  constexpr int kAH = 0, kBH = 1, kAL = 2, kBL = 3;
+  const _Float16 s16 = static_cast<_Float16>(s);
 
-  const int ktiles = Kp / kBK;
+  floatx16 acc[kSub][kSub];
 #pragma unroll
-  for (int s = 0; s < kStages - 1; ++s) issue(min(s, ktiles - 1), s);
+  for (int i = 0; i < kSub; ++i)
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) acc[i][j] = floatx16{};
+  half8 ah[kSub], al[kSub], bh[kSub], bs[kSub], bl[kSub];
 
-  const int frag_row = lane & 31;  // row (A) / column (B) inside a 32 x 32 tile
-  const int frag_kc = lane >> 5;   // which 8-wide k chunk of the 16-wide step
-  for (int kt = 0; kt < ktiles; ++kt) {
-    // Stage kt has landed for this wave once at most the (kStages - 2) later
-    // stages' DMAs are outstanding; the barrier makes it so for every wave and
-    // guarantees that no wave still reads the slot refilled just below.
-    wait_vmcnt<(kStages - 2) * kDmaPerStage>();
-    lds_barrier();
-    issue(min(kt + kStages - 1, ktiles - 1), (kt + kStages - 1) % kStages);
-    const uint16_t* s = lds + (kt % kStages) * kStage;
 #pragma unroll
-    for (int ks = 0; ks < kSteps; ++ks) {
-      const int kc = ks * 2 + frag_kc;
-      half8 ah[kSubM], al[kSubM], bh[kSubN], bl[kSubN];
+  for (int st = 0; st < S; ++st)
 #pragma unroll
-      for (int i = 0; i < kSubM; ++i) {
-        const int r = wm * kWaveM + i * 32 + frag_row;
-        const int o = r * kBK + (swizzle(r, kc) << 3);
-        ah[i] = *reinterpret_cast<const half8*>(s + kOffAH + o);
-        if constexpr (kPairs == 2) al[i] = *reinterpret_cast<const half8*>(s + kOffAL + o);
+    for (int n = 0; n < kDma; ++n) dma_one(st, n);
+  wait_vmcnt<(S - 1) * kDma>();
+  lds_barrier();
+#pragma unroll
+  for (int i = 0; i < kSub; ++i) {
+    ah[i] = rd(0, kAH, aoff[i]);
+    bh[i] = rd(0, kBH, boff[i]);
+    if constexpr (kEl) {
+      al[i] = rd(0, kAL, aoff[i]);
+      bl[i] = rd(0, kBL, boff[i]);
+      bs[i] = bh[i] * s16;
+    }
+  }
+
+  if constexpr (kEl) {
+    // One k-step: G1 = HH (A_hi x sB_hi) column by column, G2 = XA (A_lo x
+    // B_hi) row by row, G3 = XB (A_hi x B_lo) row by row, in this order for
+    // every accumulator.  The fragments of step kt+1 come from stage kt+1.
+    auto step = [&](int kt) {
+      const int nk = kt + 1;
+      int dn = 0;
+      auto dma_next = [&]() {
+        if (dn < kDma) dma_one(kt + S, dn++);
+      };
+#pragma unroll
+      for (int j = 0; j < kSub; ++j) {
+#pragma unroll
+        for (int i = 0; i < kSub; ++i) acc[i][j] = mfma32(ah[i], bs[j], acc[i][j]);
+        SCHED_FENCE();
+        if (j == 0) {
+          wait_vmcnt<(S - 2) * kDma>();
+          lds_barrier();
+        }
+        dma_next();
+        SCHED_FENCE();
       }
 #pragma unroll
-      for (int j = 0; j < kSubN; ++j) {
-        const int r = wn * kWaveN + j * 32 + frag_row;
-        const int o = r * kBK + (swizzle(r, kc) << 3);
-        bh[j] = *reinterpret_cast<const half8*>(s + kOffBH + o);
-        if constexpr (kPairs == 2) bl[j] = *reinterpret_cast<const half8*>(s + kOffBL + o);
+      for (int i = 0; i < kSub; ++i) {
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(al[i], bh[j], acc[i][j]);
+        SCHED_FENCE();
+        al[i] = rd(nk, kAL, aoff[i]);
+        dma_next();
+        SCHED_FENCE();
       }
 #pragma unroll
-      for (int i = 0; i < kSubM; ++i)
+      for (int i = 0; i < kSub; ++i) {
 #pragma unroll
-        for (int j = 0; j < kSubN; ++j) {
-          acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
-          if constexpr (V == kTermwise) {
-            xa[i][j] = mfma32(al[i], bh[j], xa[i][j]);
-            xb[i][j] = mfma32(ah[i], bl[j], xb[i][j]);
-          } else if constexpr (V == kElementwise) {
-            xa[i][j] = mfma32(al[i], bh[j], ks == 0 ? zero : xa[i][j]);
-            xb[i][j] = mfma32(ah[i], bl[j], ks == 0 ? zero : xb[i][j]);
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bl[j], acc[i][j]);
+        SCHED_FENCE();
+        ah[i] = rd(nk, kAH, aoff[i]);
+        if (i < 2) {
+          bh[2 * i] = rd(nk, kBH, boff[2 * i]);
+          bh[2 * i + 1] = rd(nk, kBH, boff[2 * i + 1]);
+        } else {
+          bs[2 * (i - 2)] = bh[2 * (i - 2)] * s16;
+          bs[2 * (i - 2) + 1] = bh[2 * (i - 2) + 1] * s16;
+        }
+        SCHED_FENCE();
+      }
+#pragma unroll
+      for (int j = 0; j < kSub; ++j) bl[j] = rd(nk, kBL, boff[j]);
+    };
+    for (int kt = 0; kt < ktiles; kt += 2) {
+      step(kt);
+      step(kt + 1);
+    }
+  } else {
+    // Hi-only: double-buffered fragments (they are few), read right after the
+    // barrier of each step.
+    half8 ah2[kSub], bh2[kSub];
+    auto step = [&](int kt, half8 (&ac)[kSub], half8 (&bc)[kSub], half8 (&an)[kSub],
+                    half8 (&bn)[kSub]) {
+#pragma unroll
+      for (int i = 0; i < kSub; ++i) {
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ac[i], bc[j], acc[i][j]);
+        SCHED_FENCE();
+        if (i == 0) {
+          wait_vmcnt<(S - 2) * kDma>();
+          lds_barrier();
+#pragma unroll
+          for (int q = 0; q < kSub; ++q) {
+            an[q] = rd(kt + 1, kAH, aoff[q]);
+            bn[q] = rd(kt + 1, kBH, boff[q]);
           }
         }
-    }
-    if constexpr (V == kElementwise) {
-      // End of block g: acc = (acc + XA_g / s) + XB_g / s.
-#pragma unroll
-      for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-        for (int j = 0; j < kSubN; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            acc[i][j][e] = __builtin_fmaf(xa[i][j][e], inv_s, acc[i][j][e]);
-            acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
-          }
+        dma_one(kt + S, i);
+        SCHED_FENCE();
+      }
+    };
+    for (int kt = 0; kt < ktiles; kt += 2) {
+      step(kt, ah, bh, ah2, bh2);
+      step(kt + 1, ah2, bh2, ah, bh);
     }
   }
   // No LDS DMA may still be writing when the workgroup retires.
   wait_vmcnt<0>();
 
-  // Epilogue: register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4 and
-  // column l%32 of its 32 x 32 tile.
-  const int col0 = tn * kBN + wn * kWaveN + (lane & 31);
-  const int row0 = tm * kBM + wm * kWaveM + (lane >> 5) * 4;
+  const float out_scale = kEl ? inv_s : 1.0f;
+  const int col0 = tn * kWide + wn * 128 + (lane & 31);
+  const int row0 = tm * kWide + wm * 128 + (lane >> 5) * 4;
+  const bool full = (tm + 1) * kWide <= M && (tn + 1) * kWide <= N;
+  store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full,
+                         [&](int i, int j, int r) { return acc[i][j][r] * out_scale; });
+}
+
+// ---------------------------------------------------------------------------
+// 256 x 128 tiles: termwise and the unscaled elementwise fallback.
+constexpr int kNarrowM = 256;
+constexpr int kNarrowN = 128;
+constexpr int kNarrowThreads = 512;
+constexpr int kNarrowStages = 4;
+constexpr size_t kNarrowLdsBytes =
+    static_cast<size_t>(kNarrowStages) * 2 * (kNarrowM + kNarrowN) * kSlice * 2;
+
+template <int V>
+__global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
+    const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
+    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
+    const int* __restrict__ range_flag, int Kp, int tiles_m, int tiles_n,
+    float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
+  static_assert(V == kElementwise || V == kTermwise, "narrow kernel variants");
+  constexpr int S = kNarrowStages;
+  constexpr int kAHalves = kNarrowM * kSlice;  // A plane slot: two tiles
+  constexpr int kBHalves = kNarrowN * kSlice;  // B plane slot: one tile
+  constexpr int kAH = 0, kAL = kAHalves, kBH = 2 * kAHalves, kBL = 2 * kAHalves + kBHalves;
+  constexpr int kStageHalves = 2 * (kAHalves + kBHalves);
+  constexpr int kDma = 3;  // 24 blocks of 1 KiB per stage over 8 waves
+  constexpr int kSub = 2;
+  if constexpr (V == kElementwise) {
+    if (!*range_flag) return;  // the scaled wide kernel handles this case
+  }
+  extern __shared__ __align__(16) uint16_t lds[];
+
+  int tm, tn;
+  tile_of<8>(tiles_m, tiles_n, tm, tn);
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  const int64_t slices = Kp / kSlice;
+  const int ktiles = static_cast<int>(slices);
+  const int64_t panel_stride = slices * kTileHalves;
+
+  // Wave w copies block w of A_hi and of A_lo (8 blocks each: two tiles of
+  // four) and block w of the eight blocks of B_hi and B_lo.
+  const uint16_t* src[3] = {
+      a_hi + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
+      a_lo + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
+      (w < 4 ? b_hi : b_lo) + tn * panel_stride + (w & 3) * 512 + lane * 8};
+  const int dst_off[3] = {kAH + w * 512, kAL + w * 512, (w < 4 ? kBH : kBL) + (w & 3) * 512};
+  const unsigned lds_base = lds_address(lds);
+  auto dma_one = [&](int kt, int n) {
+    const int ktc = min(kt, ktiles - 1);
+    dma16(src[n] + static_cast<int64_t>(ktc) * kTileHalves,
+          lds_base + ((kt % S) * kStageHalves + dst_off[n]) * 2);
+  };
+
+  const int fr = lane & 31, fk = lane >> 5;
+  int aoff[kSub], boff[kSub];
 #pragma unroll
-  for (int i = 0; i < kSubM; ++i)
+  for (int i = 0; i < kSub; ++i) {
+    aoff[i] = frag_offset(wm * 64 + i * 32 + fr, fk);
+    boff[i] = frag_offset(wn * 64 + i * 32 + fr, fk);
+  }
+  auto rd = [&](int kt, int slot, int off) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + slot + off);
+  };
+  const floatx16 zero = {};
+  floatx16 acc[kSub][kSub], xa[kSub][kSub], xb[kSub][kSub];
 #pragma unroll
-    for (int j = 0; j < kSubN; ++j) {
-      const int col = col0 + j * 32;
+  for (int i = 0; i < kSub; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = row0 + i * 32 + (r >> 2) * 8 + (r & 3);
-        float v = acc[i][j][r];
-        if constexpr (V == kTermwise) {
-          v = __builtin_fmaf(xa[i][j][r], inv_s, v);
-          v = __builtin_fmaf(xb[i][j][r], inv_s, v);
-        }
-        if (row < M && col < N) C[static_cast<size_t>(row) * ldc + col] = v;
+    for (int j = 0; j < kSub; ++j) acc[i][j] = xa[i][j] = xb[i][j] = zero;
+  half8 ah[kSub], al[kSub], bh[kSub], bl[kSub];
+
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int n = 0; n < kDma; ++n) dma_one(st, n);
+  wait_vmcnt<(S - 1) * kDma>();
+  lds_barrier();
+#pragma unroll
+  for (int i = 0; i < kSub; ++i) {
+    ah[i] = rd(0, kAH, aoff[i]);
+    al[i] = rd(0, kAL, aoff[i]);
+    bh[i] = rd(0, kBH, boff[i]);
+    bl[i] = rd(0, kBL, boff[i]);
+  }
+
+  // One k-step: XA, then HH, then XB; each fragment is reloaded with step
+  // kt+1 once its last MFMA of the step is issued.  `first` marks the first
+  // step of an elementwise block (block sums restart), `last` its end (fold).
+  auto step = [&](int kt, bool first, bool last) {
+    const int nk = kt + 1;
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+      for (int j = 0; j < kSub; ++j)
+        xa[i][j] = mfma32(al[i], bh[j], (V == kElementwise && first) ? zero : xa[i][j]);
+    SCHED_FENCE();
+    wait_vmcnt<(S - 2) * kDma>();
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < kSub; ++i) al[i] = rd(nk, kAL, aoff[i]);
+    dma_one(kt + S, 0);
+    SCHED_FENCE();
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+      for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
+    SCHED_FENCE();
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) bh[j] = rd(nk, kBH, boff[j]);
+    dma_one(kt + S, 1);
+    SCHED_FENCE();
+#pragma unroll
+    for (int i = 0; i < kSub; ++i)
+#pragma unroll
+      for (int j = 0; j < kSub; ++j)
+        xb[i][j] = mfma32(ah[i], bl[j], (V == kElementwise && first) ? zero : xb[i][j]);
+    SCHED_FENCE();
+#pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+      ah[i] = rd(nk, kAH, aoff[i]);
+      bl[i] = rd(nk, kBL, boff[i]);
+    }
+    dma_one(kt + S, 2);
+    SCHED_FENCE();
+    if constexpr (V == kElementwise) {
+      if (last) {
+        // End of block g: acc = (acc + XA_g / s) + XB_g / s.
+#pragma unroll
+        for (int i = 0; i < kSub; ++i)
+#pragma unroll
+          for (int j = 0; j < kSub; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              acc[i][j][e] = __builtin_fmaf(xa[i][j][e], inv_s, acc[i][j][e]);
+              acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
+            }
       }
     }
+  };
+  for (int kt = 0; kt < ktiles; kt += 2) {
+    step(kt, true, false);
+    step(kt + 1, false, true);
+  }
+  wait_vmcnt<0>();
+
+  const int col0 = tn * kNarrowN + wn * 64 + (lane & 31);
+  const int row0 = tm * kNarrowM + wm * 64 + (lane >> 5) * 4;
+  const bool full = (tm + 1) * kNarrowM <= M && (tn + 1) * kNarrowN <= N;
+  store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
+    float v = acc[i][j][r];
+    if constexpr (V == kTermwise) {
+      v = __builtin_fmaf(xa[i][j][r], inv_s, v);
+      v = __builtin_fmaf(xb[i][j][r], inv_s, v);
+    }
+    return v;
+  });
+}
+
+template <typename Kern>
+hipError_t set_lds(Kern kernel, size_t bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                             static_cast<int>(bytes));
 }
 
 template <int V>
-hipError_t launch_variant(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                          float inv_s, hipStream_t stream) {
-  constexpr int kPairs = (V == kHiOnly) ? 1 : 2;
-  constexpr size_t lds_bytes =
-      static_cast<size_t>(kStages) * kPairs * (kBM + kBN) * kBK * sizeof(uint16_t);
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&gemm_kernel<V>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds_bytes));
+hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
+                       hipStream_t stream) {
+  constexpr size_t lds = wide_lds_bytes<V>();
+  static const hipError_t attr = set_lds(&gemm_wide_kernel<V>, lds);
   if (attr != hipSuccess) return attr;
-  const int tiles_m = static_cast<int>(p.Mp / kBM);
-  const int tiles_n = static_cast<int>(p.Np / kBN);
-  hipLaunchKernelGGL(gemm_kernel<V>, dim3(tiles_m * tiles_n), dim3(kThreads), lds_bytes, stream,
-                     p.a_hi, p.a_lo, p.b_hi, p.b_lo, static_cast<int>(p.Kp), tiles_m, tiles_n, C,
-                     ldc, static_cast<int>(M), static_cast<int>(N), inv_s);
+  const int tiles_m = static_cast<int>(p.Mp / kWide);
+  const int tiles_n = static_cast<int>(p.Np / kWide);
+  hipLaunchKernelGGL(gemm_wide_kernel<V>, dim3(tiles_m * tiles_n), dim3(kWideThreads), lds,
+                     stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range_flag,
+                     static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
+                     static_cast<int>(N), s, 1.0f / s);
+  return hipGetLastError();
+}
+
+template <int V>
+hipError_t launch_narrow(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
+                         hipStream_t stream) {
+  static const hipError_t attr = set_lds(&gemm_narrow_kernel<V>, kNarrowLdsBytes);
+  if (attr != hipSuccess) return attr;
+  const int tiles_m = static_cast<int>(p.Mp / kNarrowM);
+  const int tiles_n = static_cast<int>(p.Np / kNarrowN);
+  hipLaunchKernelGGL(gemm_narrow_kernel<V>, dim3(tiles_m * tiles_n), dim3(kNarrowThreads),
+                     kNarrowLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range_flag,
+                     static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
+                     static_cast<int>(N), s, 1.0f / s);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                       float inv_scale, int variant, hipStream_t stream) {
+                       float scale, int variant, hipStream_t stream) {
   switch (variant) {
-    case kElementwise: return launch_variant<kElementwise>(p, M, N, C, ldc, inv_scale, stream);
-    case kTermwise: return launch_variant<kTermwise>(p, M, N, C, ldc, inv_scale, stream);
-    case kHiOnly: return launch_variant<kHiOnly>(p, M, N, C, ldc, inv_scale, stream);
+    case kElementwise: {
+      const hipError_t e = launch_wide<kElementwise>(p, M, N, C, ldc, scale, stream);
+      if (e != hipSuccess) return e;
+      return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, stream);
+    }
+    case kTermwise: return launch_narrow<kTermwise>(p, M, N, C, ldc, scale, stream);
+    case kHiOnly: return launch_wide<kHiOnly>(p, M, N, C, ldc, scale, stream);
     default: return hipErrorInvalidValue;
   }
 }

@@ -13,21 +13,41 @@ namespace sgc {
 // high-high-only baseline.
 enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2 };
 
-// GEMM tiling.  The split planes are padded to these multiples so the GEMM's
-// main loop needs no bounds checks; only the C store is masked.
-constexpr int kBM = 256;     // rows of C per workgroup
-constexpr int kBN = 128;     // columns of C per workgroup
-constexpr int kBK = 32;      // k per LDS stage; also the elementwise k-block
-constexpr int kKPad = 64;    // K is padded to a multiple of this (an even number of stages)
-constexpr int kThreads = 512;
+// Plane layout in the workspace ("panel tiles").  Every FP16 plane (A_hi,
+// A_lo, and B_hi, B_lo of B transposed) is cut into panels of kPanel rows and
+// slices of kSlice values of k; the kPanel x kSlice tile of (panel, slice) is
+// stored contiguously (4 KiB) at tile index panel * (Kp / kSlice) + slice, so
+// one k-step of a GEMM stage is a handful of contiguous 4 KiB blocks and the
+// DMA into LDS reads whole cache lines.  Inside a tile, row r holds its 16
+// values as two 16-byte chunks; chunk c is stored at position c ^ tile_swizzle(r)
+// so that the MFMA fragment reads from LDS (32 rows, one chunk each) spread
+// over all banks.  The GEMM copies tiles into LDS verbatim.
+constexpr int kPanel = 128;                     // rows per panel
+constexpr int kSlice = 16;                      // k per tile = one MFMA k-step
+constexpr int kTileHalves = kPanel * kSlice;    // 2048 halves = 4 KiB
+constexpr int kRowPad = 256;                    // M and N are padded to this
+constexpr int kKPad = 64;                       // K is padded to this
+constexpr int kFlagBytes = 256;                 // workspace header
+
+__host__ __device__ inline int tile_swizzle(int row) { return (row >> 3) & 1; }
+
+// Index (in halves) of element (row, k) of a tiled plane with Kp columns.
+__host__ __device__ inline int64_t tiled_index(int64_t row, int64_t k, int64_t Kp) {
+  const int64_t tile = (row / kPanel) * (Kp / kSlice) + k / kSlice;
+  const int r = static_cast<int>(row % kPanel);
+  const int kk = static_cast<int>(k % kSlice);
+  return tile * kTileHalves + r * kSlice + (((kk >> 3) ^ tile_swizzle(r)) << 3) + (kk & 7);
+}
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-// Layout of the split planes in the workspace.  A_hi/A_lo are Mp x Kp,
-// k-contiguous (row-major).  B_hi/B_lo hold B transposed, Np x Kp,
-// k-contiguous, so both MFMA operands read 8 consecutive k per lane.
+// Workspace: a header whose first int is the range flag, then the four
+// planes.  A planes are Mp x Kp, B planes Np x Kp (B transposed), all tiled.
+// range_flag != 0 after the split of B when some |B_hi| * s exceeds the
+// largest finite FP16 value (the scaled elementwise kernel cannot be used).
 struct Planes {
   int64_t Mp, Np, Kp;
+  int* range_flag;
   uint16_t* a_hi;
   uint16_t* a_lo;
   uint16_t* b_hi;
@@ -38,24 +58,32 @@ struct Planes {
 Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base);
 
 // Enqueue the split of a rows x cols row-major FP32 matrix into row-major
-// hi/lo planes with leading dimension ldh, writing zeros in the padding
-// [rows, rows_pad) x [0, cols_pad) and [0, rows) x [cols, cols_pad).
+// hi/lo planes with leading dimension ldh (the public split entry point).
 hipError_t launch_split_rows(int64_t rows, int64_t cols, const float* X, int64_t ldx,
-                             uint16_t* hi, uint16_t* lo, int64_t ldh, int64_t rows_pad,
-                             int64_t cols_pad, float scale, hipStream_t stream);
+                             uint16_t* hi, uint16_t* lo, int64_t ldh, float scale,
+                             hipStream_t stream);
 
-// Enqueue the split of a K x N row-major FP32 matrix B into TRANSPOSED
-// planes (Np x Kp, k-contiguous), zero-padded.
-hipError_t launch_split_cols_transposed(int64_t K, int64_t N, const float* B, int64_t ldb,
-                                        uint16_t* hi_t, uint16_t* lo_t, int64_t Np,
-                                        int64_t Kp, float scale, hipStream_t stream);
+// Enqueue the split of A (M x K row-major) into the tiled A planes,
+// zero-filling the padding up to Mp x Kp.
+hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
+                          float scale, hipStream_t stream);
 
-// Enqueue the three-product MFMA GEMM on prepared planes.
+// Enqueue the split of B (K x N row-major) into the tiled, transposed B
+// planes (Np x Kp), zero-filling the padding, and recompute the range flag.
+hipError_t launch_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
+                          float scale, hipStream_t stream);
+
+// Enqueue the MFMA GEMM on prepared planes.
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                       float inv_scale, int variant, hipStream_t stream);
+                       float scale, int variant, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);
+
+// The elementwise k-block of the scaled kernel (one MFMA k-step) and of the
+// fallback kernel used when the range flag is set.
+constexpr int kBlockScaled = kSlice;
+constexpr int kBlockFallback = 2 * kSlice;
 
 }  // namespace sgc

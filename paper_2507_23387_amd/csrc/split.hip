@@ -10,12 +10,14 @@
 //   - the compiler may fuse r * s and the conversion into v_fma_mixlo_f16,
 //     which rounds once; r * s is exact because s is a power of two (checked
 //     by the C-ABI), so this equals the two-step definition bit for bit.
-// Both kernels are HBM-bound elementwise passes: 4 B read and 4 B written
-// (hi + lo) per element.
+// All split kernels are HBM-bound elementwise passes: 4 B read and 4 B
+// written (hi + lo) per element.
 #include "internal.h"
 
 namespace sgc {
 namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void split_value(float a, float s, uint16_t& hi, uint16_t& lo) {
   const _Float16 h = static_cast<_Float16>(a);
@@ -67,53 +69,105 @@ __global__ __launch_bounds__(256) void split_rows_kernel(
   }
 }
 
-// Transposing split of B (K x N row-major) into Np x Kp k-contiguous planes.
-// A 64 (k) x 64 (n) tile per workgroup: coalesced row reads along n, split in
-// registers, transpose through LDS, coalesced 32-byte row writes along k.
-__global__ __launch_bounds__(256) void split_cols_t_kernel(
-    int64_t K, int64_t N, const float* __restrict__ B, int64_t ldb,
-    uint16_t* __restrict__ hi_t, uint16_t* __restrict__ lo_t, int64_t Kp, float s) {
-  constexpr int kPitch = 66;  // halves per LDS row (64 + 2): spreads banks
-  __shared__ uint16_t sh[64 * kPitch];
-  __shared__ uint16_t sl[64 * kPitch];
-  const int64_t k0 = static_cast<int64_t>(blockIdx.x) * 64;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.y) * 64;
-  const int t = threadIdx.x;
-  {
-    const int n = t & 63;
-    const int kq = t >> 6;
-    const int64_t gn = n0 + n;
-#pragma unroll 4
-    for (int r = 0; r < 16; ++r) {
-      const int k = kq + 4 * r;
-      const int64_t gk = k0 + k;
-      const float a = (gk < K && gn < N) ? B[gk * ldb + gn] : 0.0f;
-      uint16_t h, l;
-      split_value(a, s, h, l);
-      sh[n * kPitch + k] = h;
-      sl[n * kPitch + k] = l;
+// Split of A into the tiled planes.  Thread = 8 consecutive k of one row (one
+// 16-byte chunk of each output plane); a workgroup covers 4 rows x 512 k, so
+// each wave reads 2 KiB of one row contiguously and the four rows of a
+// workgroup complete every 128-byte line they write.  blockIdx.y strides
+// over row quads.
+template <bool kVec>
+__global__ __launch_bounds__(256) void split_a_tiled_kernel(
+    int64_t M, int64_t K, const float* __restrict__ X, int64_t ldx, uint16_t* __restrict__ hi,
+    uint16_t* __restrict__ lo, int64_t Mp, int64_t Kp, float s) {
+  const int64_t k0 = (static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63)) * 8;
+  if (k0 >= Kp) return;
+  for (int64_t m = static_cast<int64_t>(blockIdx.y) * 4 + (threadIdx.x >> 6); m < Mp;
+       m += static_cast<int64_t>(gridDim.y) * 4) {
+    float v[8];
+    if (kVec && m < M && k0 + 7 < K) {
+      const float4* src = reinterpret_cast<const float4*>(X + m * ldx + k0);
+      const float4 f0 = src[0], f1 = src[1];
+      v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
+      v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? X[m * ldx + k0 + e] : 0.0f;
     }
+    u32x4 hv, lv;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      uint16_t h0, l0, h1, l1;
+      split_value(v[2 * e], s, h0, l0);
+      split_value(v[2 * e + 1], s, h1, l1);
+      hv[e] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+      lv[e] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+    }
+    const int64_t idx = tiled_index(m, k0, Kp);
+    *reinterpret_cast<u32x4*>(hi + idx) = hv;
+    *reinterpret_cast<u32x4*>(lo + idx) = lv;
+  }
+}
+
+// Split of B (K x N row-major) into the tiled planes of B transposed.  One
+// workgroup = one 128 (n) x 16 (k) tile: thread t reads 8 consecutive n of
+// row k = t / 16 (each wave reads four 512-byte row pieces), the split values
+// are transposed through LDS, and thread t writes 16-byte chunk t of the 4 KiB
+// tile of each plane.  It also raises the range flag when some
+// |B_hi| * s > 65504 (the largest finite FP16 value).
+template <bool kVec>
+__global__ __launch_bounds__(256) void split_b_tiled_kernel(
+    int64_t K, int64_t N, const float* __restrict__ B, int64_t ldb, uint16_t* __restrict__ hi,
+    uint16_t* __restrict__ lo, int64_t Kp, float s, int* __restrict__ range_flag) {
+  constexpr int kPitch = kSlice + 2;  // halves per LDS row: 36 bytes spread the banks
+  __shared__ uint16_t sh[kPanel * kPitch];
+  __shared__ uint16_t sl[kPanel * kPitch];
+  const int t = threadIdx.x;
+  const int64_t slice = blockIdx.x;
+  const int64_t panel = blockIdx.y;
+  {
+    const int kl = t >> 4;
+    const int nl = (t & 15) * 8;
+    const int64_t k = slice * kSlice + kl;
+    const int64_t n = panel * kPanel + nl;
+    float v[8];
+    if (kVec && k < K && n + 7 < N) {
+      const float4* src = reinterpret_cast<const float4*>(B + k * ldb + n);
+      const float4 f0 = src[0], f1 = src[1];
+      v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
+      v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (k < K && n + e < N) ? B[k * ldb + n + e] : 0.0f;
+    }
+    bool big = false;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint16_t h, l;
+      split_value(v[e], s, h, l);
+      big |= __builtin_fabsf(static_cast<float>(__builtin_bit_cast(_Float16, h))) * s > 65504.0f;
+      sh[(nl + e) * kPitch + kl] = h;
+      sl[(nl + e) * kPitch + kl] = l;
+    }
+    if (big) *range_flag = 1;
   }
   __syncthreads();
   {
-    const int n = t >> 2;
-    const int kc = (t & 3) * 16;
-    uint32_t hv[8], lv[8];
+    const int r = t >> 1;
+    const int c = (t & 1) ^ tile_swizzle(r);  // logical chunk stored at position t & 1
+    const uint16_t* hrow = sh + r * kPitch + c * 8;
+    const uint16_t* lrow = sl + r * kPitch + c * 8;
+    u32x4 hv, lv;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      hv[e] = static_cast<uint32_t>(sh[n * kPitch + kc + 2 * e]) |
-              (static_cast<uint32_t>(sh[n * kPitch + kc + 2 * e + 1]) << 16);
-      lv[e] = static_cast<uint32_t>(sl[n * kPitch + kc + 2 * e]) |
-              (static_cast<uint32_t>(sl[n * kPitch + kc + 2 * e + 1]) << 16);
+    for (int e = 0; e < 4; ++e) {
+      hv[e] = static_cast<uint32_t>(hrow[2 * e]) | (static_cast<uint32_t>(hrow[2 * e + 1]) << 16);
+      lv[e] = static_cast<uint32_t>(lrow[2 * e]) | (static_cast<uint32_t>(lrow[2 * e + 1]) << 16);
     }
-    uint4* hdst = reinterpret_cast<uint4*>(hi_t + (n0 + n) * Kp + k0 + kc);
-    uint4* ldst = reinterpret_cast<uint4*>(lo_t + (n0 + n) * Kp + k0 + kc);
-    hdst[0] = uint4{hv[0], hv[1], hv[2], hv[3]};
-    hdst[1] = uint4{hv[4], hv[5], hv[6], hv[7]};
-    ldst[0] = uint4{lv[0], lv[1], lv[2], lv[3]};
-    ldst[1] = uint4{lv[4], lv[5], lv[6], lv[7]};
+    const int64_t base = (panel * (Kp / kSlice) + slice) * kTileHalves + t * 8;
+    *reinterpret_cast<u32x4*>(hi + base) = hv;
+    *reinterpret_cast<u32x4*>(lo + base) = lv;
   }
 }
+
+__global__ void flag_reset_kernel(int* range_flag) { *range_flag = 0; }
 
 __global__ __launch_bounds__(256) void zero_kernel(int64_t M, int64_t N, float* __restrict__ C,
                                                    int64_t ldc) {
@@ -129,30 +183,52 @@ inline unsigned grid_rows(int64_t rows) {
 }  // namespace
 
 hipError_t launch_split_rows(int64_t rows, int64_t cols, const float* X, int64_t ldx,
-                             uint16_t* hi, uint16_t* lo, int64_t ldh, int64_t rows_pad,
-                             int64_t cols_pad, float scale, hipStream_t stream) {
-  if (rows_pad <= 0 || cols_pad <= 0) return hipSuccess;
-  const int64_t quads = (cols_pad + 3) / 4;
-  const dim3 grid(static_cast<unsigned>((quads + 255) / 256), grid_rows(rows_pad));
+                             uint16_t* hi, uint16_t* lo, int64_t ldh, float scale,
+                             hipStream_t stream) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  const int64_t quads = (cols + 3) / 4;
+  const dim3 grid(static_cast<unsigned>((quads + 255) / 256), grid_rows(rows));
   const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) && (ldx % 4 == 0) &&
                    (reinterpret_cast<uintptr_t>(hi) % 8 == 0) &&
                    (reinterpret_cast<uintptr_t>(lo) % 8 == 0) && (ldh % 4 == 0);
   if (vec)
     hipLaunchKernelGGL(split_rows_kernel<true>, grid, dim3(256), 0, stream, rows, cols, X, ldx,
-                       hi, lo, ldh, rows_pad, cols_pad, scale);
+                       hi, lo, ldh, rows, cols, scale);
   else
     hipLaunchKernelGGL(split_rows_kernel<false>, grid, dim3(256), 0, stream, rows, cols, X, ldx,
-                       hi, lo, ldh, rows_pad, cols_pad, scale);
+                       hi, lo, ldh, rows, cols, scale);
   return hipGetLastError();
 }
 
-hipError_t launch_split_cols_transposed(int64_t K, int64_t N, const float* B, int64_t ldb,
-                                        uint16_t* hi_t, uint16_t* lo_t, int64_t Np,
-                                        int64_t Kp, float scale, hipStream_t stream) {
-  // Np and Kp are multiples of 64 (plan_planes pads them to the GEMM tiles).
-  const dim3 grid(static_cast<unsigned>(Kp / 64), static_cast<unsigned>(Np / 64));
-  hipLaunchKernelGGL(split_cols_t_kernel, grid, dim3(256), 0, stream, K, N, B, ldb, hi_t, lo_t,
-                     Kp, scale);
+hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
+                          float scale, hipStream_t stream) {
+  // Mp is a multiple of 256 and Kp of 64 (plan_planes).
+  const dim3 grid(static_cast<unsigned>((p.Kp + 511) / 512), grid_rows(p.Mp / 4));
+  const bool vec = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (lda % 4 == 0);
+  if (vec)
+    hipLaunchKernelGGL(split_a_tiled_kernel<true>, grid, dim3(256), 0, stream, M, K, A, lda,
+                       p.a_hi, p.a_lo, p.Mp, p.Kp, scale);
+  else
+    hipLaunchKernelGGL(split_a_tiled_kernel<false>, grid, dim3(256), 0, stream, M, K, A, lda,
+                       p.a_hi, p.a_lo, p.Mp, p.Kp, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
+                          float scale, hipStream_t stream) {
+  hipLaunchKernelGGL(flag_reset_kernel, dim3(1), dim3(1), 0, stream, p.range_flag);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // One workgroup per tile: Kp / 16 slices x Np / 128 panels (Np / 128 <= 65535
+  // is checked by the C-ABI).
+  const dim3 grid(static_cast<unsigned>(p.Kp / kSlice), static_cast<unsigned>(p.Np / kPanel));
+  const bool vec = (reinterpret_cast<uintptr_t>(B) % 16 == 0) && (ldb % 4 == 0);
+  if (vec)
+    hipLaunchKernelGGL(split_b_tiled_kernel<true>, grid, dim3(256), 0, stream, K, N, B, ldb,
+                       p.b_hi, p.b_lo, p.Kp, scale, p.range_flag);
+  else
+    hipLaunchKernelGGL(split_b_tiled_kernel<false>, grid, dim3(256), 0, stream, K, N, B, ldb,
+                       p.b_hi, p.b_lo, p.Kp, scale, p.range_flag);
   return hipGetLastError();
 }
 

@@ -46,13 +46,14 @@ def test_status_strings(lib):
 
 
 def test_block_k(lib):
-    assert lib.sgemm_cube_block_k() == 32
+    assert lib.sgemm_cube_block_k() == 16
 
 
 def test_workspace_size(lib):
-    # four FP16 planes: A padded to 256-row tiles, B to 128-column tiles, K to 64
-    assert lib.sgemm_cube_workspace_size(8192, 8192, 8192) == 4 * 8192 * 8192 * 2
-    assert lib.sgemm_cube_workspace_size(1, 1, 1) == 2 * (256 * 64 * 2) + 2 * (128 * 64 * 2)
+    # 256-byte header (range flag), then four FP16 planes padded to 256 rows x 64 k.
+    assert lib.sgemm_cube_workspace_size(8192, 8192, 8192) == 256 + 4 * 8192 * 8192 * 2
+    assert lib.sgemm_cube_workspace_size(1, 1, 1) == 256 + 4 * (256 * 64 * 2)
+    assert lib.sgemm_cube_workspace_size(300, 1, 65) == 256 + 2 * (512 * 128 * 2) + 2 * (256 * 128 * 2)
     assert lib.sgemm_cube_workspace_size(0, 5, 5) == 0
     assert lib.sgemm_cube_workspace_size(5, 5, 0) == 0
     assert lib.sgemm_cube_workspace_size(-1, 5, 5) == 0

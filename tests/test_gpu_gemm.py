@@ -2,9 +2,10 @@
 
 Bar: |C_gpu - C_oracle|_ij <= 2 K 2^-24 (|A||B|)_ij for every compared entry,
 equality where (|A||B|)_ij = 0, identical inf/NaN patterns.  The oracle runs
-with the GPU's elementwise block size (sgemm_cube_block_k() = 64), so both
-sides fold the same blocks g of Eq. elementwise; only the summation order
-inside a block differs (MFMA versus sequential).
+with the GPU's elementwise block size (sgemm_cube_block_k() = 16), so both
+sides fold the same blocks g of Eq. elementwise; the summation inside a block
+differs (MFMA versus sequential, and on the scaled path each block term is
+rounded together with the accumulator), which the bar covers.
 
 Small and ragged shapes are compared in full; the five workloads at their full
 size are compared on sampled rows (each output row needs only its row of A
@@ -15,7 +16,7 @@ import pytest
 import oracle
 import workloads
 from oracle import bounds
-from tests.gpu_util import gemm, hgemm, log, padded, to_dev
+from tests.gpu_util import gemm, hgemm, log, padded, split, to_dev
 from tests.helpers import abs_ab, assert_parity, ref64
 
 pytestmark = pytest.mark.gpu
@@ -119,6 +120,120 @@ def test_non_finite_inputs_propagate_like_the_oracle(gpu, order):
     assert np.isnan(Co).any()
 
 
+def test_non_finite_inputs_on_the_scaled_elementwise_path(gpu):
+    """The same special values with B kept inside the scaled kernel's range
+    (|B_hi| s <= 65504), A carrying the hi and lo overflows instead."""
+    M, N, K = 40, 50, 70
+    A, B = workloads.make_operands(M, N, K, 19, "uniform_pm1")
+    A[3, 5] = 70000.0      # hi overflows
+    A[7, 9] = -np.inf
+    A[20, 21] = 32784.0    # lo overflows with s = 2^12
+    B[11, 13] = np.nan
+    log("gemm non-finite, scaled elementwise path")
+    C = gemm(A, B, 4096.0, "elementwise")
+    Co = oracle.sgemm(A, B, 4096.0, "elementwise", kb=_kb())
+    assert_parity(C, Co, K, abs_ab(A, B), "non-finite scaled")
+    assert np.isnan(Co).any() and np.isinf(Co).any()
+
+
+@pytest.mark.parametrize("edge", ["scaled_limit", "fallback"])
+def test_elementwise_range_switch(gpu, edge):
+    """The scaled elementwise kernel needs s * B_hi to stay finite in FP16.
+    B's largest hi exactly at 65504 / s keeps it; one FP16 ulp above switches
+    to the unscaled fallback.  Both meet the bar, on ragged shapes."""
+    M, N, K = 300, 260, 257
+    A, B = workloads.make_operands(M, N, K, 21, "uniform_pm1")
+    B[5, 7] = 31.984375 if edge == "scaled_limit" else 32.0   # x 2^11 = 65504 or 65536
+    log(f"gemm elementwise range switch {edge}")
+    C = gemm(A, B, 2048.0, "elementwise")
+    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
+    assert_parity(C, Co, K, abs_ab(A, B), f"range switch {edge}")
+
+
+def _range_flag(ws):
+    """The range flag is the first int of the workspace header."""
+    import torch
+
+    return int(ws[:4].view(torch.int32).item())
+
+
+def test_range_flag_follows_the_last_split_of_b(gpu):
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K = 70, 90, 33
+    A, B = workloads.make_operands(M, N, K, 23, "uniform_pm1")
+    Bbig = B.copy()
+    Bbig[0, 0] = 40.0
+    dA, dB, dBbig = to_dev(A), to_dev(B), to_dev(Bbig)
+    ws = binding.workspace(M, N, K)
+    nbytes = ws.numel()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def prep(a, b):
+        assert binding.sgemm_cube_prepare(M, N, K, a.data_ptr() if a is not None else 0, K,
+                                          b.data_ptr() if b is not None else 0, N, 2048.0,
+                                          ws.data_ptr(), nbytes, stream) == 0
+        torch.cuda.synchronize()
+
+    log("range flag")
+    prep(dA, dBbig)
+    assert _range_flag(ws) == 1
+    prep(dA, dB)
+    assert _range_flag(ws) == 0
+    prep(None, dBbig)
+    assert _range_flag(ws) == 1
+    prep(dA, None)            # re-splitting A alone keeps the flag of the B planes
+    assert _range_flag(ws) == 1
+
+
+def _untile(buf: np.ndarray, rows_p: int, Kp: int) -> np.ndarray:
+    """Decode a plane stored as 128-row x 16-k tiles (row r's two 8-value
+    chunks swapped when bit 3 of r is set) into a rows_p x Kp array."""
+    r = np.arange(rows_p)[:, None]
+    k = np.arange(Kp)[None, :]
+    tile = (r // 128) * (Kp // 16) + k // 16
+    rr, kk = r % 128, k % 16
+    idx = tile * 2048 + rr * 16 + (((kk >> 3) ^ ((rr >> 3) & 1)) << 3) + (kk & 7)
+    return buf[idx]
+
+
+def test_prepared_planes_match_the_split_bit_for_bit(gpu):
+    """The tiled planes written by sgemm_cube_prepare hold exactly the bits of
+    the row-major split (A) and of the split of B, transposed, with zeros in
+    the padding."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K, s = 300, 200, 100, 1024.0
+    A, B = workloads.make_operands(M, N, K, 29, "normal")
+    dA, dB = to_dev(A), to_dev(B)
+    ws = binding.workspace(M, N, K)
+    stream = torch.cuda.current_stream().cuda_stream
+    log("tiled planes vs split")
+    assert binding.sgemm_cube_prepare(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, s,
+                                      ws.data_ptr(), ws.numel(), stream) == 0
+    torch.cuda.synchronize()
+    raw = ws.cpu().numpy()
+    Mp, Np, Kp = 512, 256, 128
+    a_bytes, b_bytes = Mp * Kp * 2, Np * Kp * 2
+    planes = []
+    off = 256
+    for nbytes in (a_bytes, a_bytes, b_bytes, b_bytes):
+        planes.append(raw[off:off + nbytes].view(np.uint16))
+        off += nbytes
+    a_hi, a_lo = (_untile(p, Mp, Kp) for p in planes[:2])
+    b_hi, b_lo = (_untile(p, Np, Kp) for p in planes[2:])
+    ah, al = split(A, s)
+    bh, bl = split(B, s)
+    for got, want, rows, cols in ((a_hi, ah, M, K), (a_lo, al, M, K),
+                                  (b_hi, bh.T, N, K), (b_lo, bl.T, N, K)):
+        assert np.array_equal(got[:rows, :cols], want)
+        assert not got[rows:].any() and not got[:, cols:].any()
+
+
 def test_subnormal_fp16_products_exact(gpu):
     """FP16-subnormal operands (the 2^-14-scaled workload's regime): with
     exactly representable FP16 inputs whose products and sums are exact in
@@ -131,9 +246,10 @@ def test_subnormal_fp16_products_exact(gpu):
     log("hgemm subnormal exact")
     C = hgemm(A, B)
     assert np.array_equal(C.astype(np.float64), ref64(A, B))
-    log("sgemm subnormal exact")
-    C2 = gemm(A, B, 2048.0, "termwise")
-    assert np.array_equal(C2.astype(np.float64), ref64(A, B))
+    for order in ORDERS:
+        log(f"sgemm subnormal exact {order}")
+        C2 = gemm(A, B, 2048.0, order)
+        assert np.array_equal(C2.astype(np.float64), ref64(A, B))
 
 
 def test_deterministic_and_entry_points_agree(gpu):
