@@ -19,7 +19,7 @@ Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base) {
   const size_t a_bytes = static_cast<size_t>(round_up(p.Mp * p.Kp * 2, 256));
   const size_t b_bytes = static_cast<size_t>(round_up(p.Np * p.Kp * 2, 256));
   char* c = static_cast<char*>(base);
-  p.range_flag = reinterpret_cast<int*>(c);
+  p.range = reinterpret_cast<uint32_t*>(c);
   c += kFlagBytes;
   p.a_hi = reinterpret_cast<uint16_t*>(c);
   p.a_lo = reinterpret_cast<uint16_t*>(c + a_bytes);
@@ -83,6 +83,29 @@ int validate_gemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
   return SGEMM_CUBE_OK;
 }
 
+// A fresh stamp for every split of B (see launch_split_b); 0 is skipped.
+std::atomic<uint32_t> g_stamp{0};
+uint32_t next_stamp() {
+  uint32_t s = g_stamp.fetch_add(1, std::memory_order_relaxed) + 1;
+  return s ? s : g_stamp.fetch_add(1, std::memory_order_relaxed) + 1;
+}
+
+// Compute units of the current device, cached per device.
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices] = {};
+int current_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int n = g_cus[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    g_cus[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
 size_t ws_size(int64_t M, int64_t N, int64_t K) {
   if (M == 0 || N == 0 || K == 0) return 0;
   return plan_planes(M, N, K, nullptr).bytes;
@@ -97,8 +120,9 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
                                                                      : SGEMM_CUBE_ERR_HIP;
   const Planes p = plan_planes(M, N, K, ws);
   if (launch_split_a(p, M, K, A, lda, scale, stream) != hipSuccess) return SGEMM_CUBE_ERR_HIP;
-  if (launch_split_b(p, K, N, B, ldb, scale, stream) != hipSuccess) return SGEMM_CUBE_ERR_HIP;
-  if (launch_gemm(p, M, N, C, ldc, scale, variant, stream) != hipSuccess)
+  if (launch_split_b(p, K, N, B, ldb, scale, next_stamp(), stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (launch_gemm(p, M, N, C, ldc, scale, variant, current_cus(), stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   return SGEMM_CUBE_OK;
 }
@@ -107,7 +131,6 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
 // the allocating entry points.  The release threshold is raised so memory
 // freed at the end of a call is reused by the next one instead of going back
 // to the driver at every synchronisation.
-constexpr int kMaxDevices = 64;
 std::mutex g_pool_mu;
 hipMemPool_t g_pools[kMaxDevices] = {};
 
@@ -205,7 +228,7 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
   const sgc::Planes p = sgc::plan_planes(M, N, K, ws);
   if (A && sgc::launch_split_a(p, M, K, A, lda, scale, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
-  if (B && sgc::launch_split_b(p, K, N, B, ldb, scale, stream) != hipSuccess)
+  if (B && sgc::launch_split_b(p, K, N, B, ldb, scale, sgc::next_stamp(), stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   return SGEMM_CUBE_OK;
 }
@@ -229,7 +252,8 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
   if (sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   const sgc::Planes p = sgc::plan_planes(M, N, K, const_cast<void*>(ws));
-  return sgc::launch_gemm(p, M, N, C, ldc, scale, accum_order, stream) == hipSuccess
+  return sgc::launch_gemm(p, M, N, C, ldc, scale, accum_order, sgc::current_cus(), stream) ==
+                 hipSuccess
              ? SGEMM_CUBE_OK
              : SGEMM_CUBE_ERR_HIP;
 }

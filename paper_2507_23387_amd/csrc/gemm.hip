@@ -46,6 +46,8 @@
 // instructions.  One s_barrier per step both publishes stage kt+1 and retires
 // the slot of stage kt before it is refilled.  Past the last stage the loads
 // repeat the last stage, so every wait count is a compile-time constant.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace sgc {
@@ -98,14 +100,15 @@ __device__ __forceinline__ unsigned lds_address(const uint16_t* p) {
   return static_cast<unsigned>((uintptr_t)((__attribute__((address_space(3))) const uint16_t*)p));
 }
 
-// Map the hardware workgroup id to a (tile_m, tile_n) pair.  Workgroups are
-// dispatched round-robin over the 8 XCDs; renumbering gives each XCD a
-// contiguous range of logical tiles, and grouping kGroup tile-rows keeps the A
-// and B panels a group touches resident in that XCD's L2.
+// Map a tile index to a (tile_m, tile_n) pair.  Workgroups are dispatched
+// round-robin over the 8 XCDs, so index i runs on XCD i % 8 (also for the
+// persistent grid, whose size is a multiple of 8); renumbering gives each XCD
+// a contiguous range of logical tiles, and grouping kGroup tile-rows keeps the
+// A and B panels a group touches resident in that XCD's L2.
 template <int kGroup>
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ void tile_of(int index, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nwg = tiles_m * tiles_n;
-  int wg = blockIdx.x;
+  int wg = index;
   if ((nwg & 7) == 0) wg = (wg & 7) * (nwg >> 3) + (wg >> 3);
   const int per_group = kGroup * tiles_n;
   const int group = wg / per_group;
@@ -165,7 +168,7 @@ template <int V>
 __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
-    const int* __restrict__ range_flag, int Kp, int tiles_m, int tiles_n,
+    const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
   static_assert(V == kElementwise || V == kHiOnly, "wide kernel variants");
   constexpr bool kEl = V == kElementwise;
@@ -176,12 +179,12 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   constexpr int kDma = kPlanes * 2;               // 1 KiB DMAs per wave per stage
   constexpr int kSub = 4;                         // 32 x 32 MFMA tiles per wave side
   if constexpr (kEl) {
-    if (*range_flag) return;  // |B_hi| s overflows FP16: the narrow kernel runs instead
+    if (range[0] == range[1]) return;  // s B_hi overflows FP16: the narrow kernel runs instead
   }
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
-  tile_of<4>(tiles_m, tiles_n, tm, tn);
+  tile_of<4>(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
@@ -243,9 +246,11 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   }
 
   if constexpr (kEl) {
-    // One k-step: G1 = HH (A_hi x sB_hi) column by column, G2 = XA (A_lo x
-    // B_hi) row by row, G3 = XB (A_hi x B_lo) row by row, in this order for
-    // every accumulator.  The fragments of step kt+1 come from stage kt+1.
+    // One k-step: G1 = HH (A_hi x sB_hi), G2 = XA (A_lo x B_hi), G3 = XB
+    // (A_hi x B_lo), each row by row, in this order for every accumulator.
+    // The fragments of step kt+1 come from stage kt+1; A_hi row i is
+    // reloaded after its last use in G3 and first needed again 12 MFMAs later,
+    // in row i of the next G1.
     auto step = [&](int kt) {
       const int nk = kt + 1;
       int dn = 0;
@@ -253,11 +258,11 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
         if (dn < kDma) dma_one(kt + S, dn++);
       };
 #pragma unroll
-      for (int j = 0; j < kSub; ++j) {
+      for (int i = 0; i < kSub; ++i) {
 #pragma unroll
-        for (int i = 0; i < kSub; ++i) acc[i][j] = mfma32(ah[i], bs[j], acc[i][j]);
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bs[j], acc[i][j]);
         SCHED_FENCE();
-        if (j == 0) {
+        if (i == 0) {
           wait_vmcnt<(S - 2) * kDma>();
           lds_barrier();
         }
@@ -348,7 +353,7 @@ template <int V>
 __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
-    const int* __restrict__ range_flag, int Kp, int tiles_m, int tiles_n,
+    const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
   static_assert(V == kElementwise || V == kTermwise, "narrow kernel variants");
   constexpr int S = kNarrowStages;
@@ -359,136 +364,141 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
   constexpr int kDma = 3;  // 24 blocks of 1 KiB per stage over 8 waves
   constexpr int kSub = 2;
   if constexpr (V == kElementwise) {
-    if (!*range_flag) return;  // the scaled wide kernel handles this case
+    if (range[0] != range[1]) return;  // the scaled wide kernel handles this case
   }
   extern __shared__ __align__(16) uint16_t lds[];
 
-  int tm, tn;
-  tile_of<8>(tiles_m, tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
-  const int64_t slices = Kp / kSlice;
-  const int ktiles = static_cast<int>(slices);
-  const int64_t panel_stride = slices * kTileHalves;
-
-  // Wave w copies block w of A_hi and of A_lo (8 blocks each: two tiles of
-  // four) and block w of the eight blocks of B_hi and B_lo.
-  const uint16_t* src[3] = {
-      a_hi + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
-      a_lo + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
-      (w < 4 ? b_hi : b_lo) + tn * panel_stride + (w & 3) * 512 + lane * 8};
-  const int dst_off[3] = {kAH + w * 512, kAL + w * 512, (w < 4 ? kBH : kBL) + (w & 3) * 512};
-  const unsigned lds_base = lds_address(lds);
-  auto dma_one = [&](int kt, int n) {
-    const int ktc = min(kt, ktiles - 1);
-    dma16(src[n] + static_cast<int64_t>(ktc) * kTileHalves,
-          lds_base + ((kt % S) * kStageHalves + dst_off[n]) * 2);
-  };
-
-  const int fr = lane & 31, fk = lane >> 5;
-  int aoff[kSub], boff[kSub];
-#pragma unroll
-  for (int i = 0; i < kSub; ++i) {
-    aoff[i] = frag_offset(wm * 64 + i * 32 + fr, fk);
-    boff[i] = frag_offset(wn * 64 + i * 32 + fr, fk);
-  }
-  auto rd = [&](int kt, int slot, int off) -> half8 {
-    return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + slot + off);
-  };
-  const floatx16 zero = {};
-  floatx16 acc[kSub][kSub], xa[kSub][kSub], xb[kSub][kSub];
-#pragma unroll
-  for (int i = 0; i < kSub; ++i)
-#pragma unroll
-    for (int j = 0; j < kSub; ++j) acc[i][j] = xa[i][j] = xb[i][j] = zero;
-  half8 ah[kSub], al[kSub], bh[kSub], bl[kSub];
-
-#pragma unroll
-  for (int st = 0; st < S; ++st)
-#pragma unroll
-    for (int n = 0; n < kDma; ++n) dma_one(st, n);
-  wait_vmcnt<(S - 1) * kDma>();
-  lds_barrier();
-#pragma unroll
-  for (int i = 0; i < kSub; ++i) {
-    ah[i] = rd(0, kAH, aoff[i]);
-    al[i] = rd(0, kAL, aoff[i]);
-    bh[i] = rd(0, kBH, boff[i]);
-    bl[i] = rd(0, kBL, boff[i]);
-  }
-
-  // One k-step: XA, then HH, then XB; each fragment is reloaded with step
-  // kt+1 once its last MFMA of the step is issued.  `first` marks the first
-  // step of an elementwise block (block sums restart), `last` its end (fold).
-  auto step = [&](int kt, bool first, bool last) {
-    const int nk = kt + 1;
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-      for (int j = 0; j < kSub; ++j)
-        xa[i][j] = mfma32(al[i], bh[j], (V == kElementwise && first) ? zero : xa[i][j]);
-    SCHED_FENCE();
-    wait_vmcnt<(S - 2) * kDma>();
+  // Persistent grid: each workgroup walks tiles blockIdx.x, + gridDim.x, ...
+  for (int tile = blockIdx.x; tile < tiles_m * tiles_n; tile += gridDim.x) {
+    int tm, tn;
+    tile_of<8>(tile, tiles_m, tiles_n, tm, tn);
+    // Every wave is done with the previous tile's LDS before it is refilled.
     lds_barrier();
-#pragma unroll
-    for (int i = 0; i < kSub; ++i) al[i] = rd(nk, kAL, aoff[i]);
-    dma_one(kt + S, 0);
-    SCHED_FENCE();
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-      for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
-    SCHED_FENCE();
-#pragma unroll
-    for (int j = 0; j < kSub; ++j) bh[j] = rd(nk, kBH, boff[j]);
-    dma_one(kt + S, 1);
-    SCHED_FENCE();
-#pragma unroll
-    for (int i = 0; i < kSub; ++i)
-#pragma unroll
-      for (int j = 0; j < kSub; ++j)
-        xb[i][j] = mfma32(ah[i], bl[j], (V == kElementwise && first) ? zero : xb[i][j]);
-    SCHED_FENCE();
-#pragma unroll
-    for (int i = 0; i < kSub; ++i) {
-      ah[i] = rd(nk, kAH, aoff[i]);
-      bl[i] = rd(nk, kBL, boff[i]);
-    }
-    dma_one(kt + S, 2);
-    SCHED_FENCE();
-    if constexpr (V == kElementwise) {
-      if (last) {
-        // End of block g: acc = (acc + XA_g / s) + XB_g / s.
-#pragma unroll
-        for (int i = 0; i < kSub; ++i)
-#pragma unroll
-          for (int j = 0; j < kSub; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              acc[i][j][e] = __builtin_fmaf(xa[i][j][e], inv_s, acc[i][j][e]);
-              acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
-            }
-      }
-    }
-  };
-  for (int kt = 0; kt < ktiles; kt += 2) {
-    step(kt, true, false);
-    step(kt + 1, false, true);
-  }
-  wait_vmcnt<0>();
+    const int64_t slices = Kp / kSlice;
+    const int ktiles = static_cast<int>(slices);
+    const int64_t panel_stride = slices * kTileHalves;
 
-  const int col0 = tn * kNarrowN + wn * 64 + (lane & 31);
-  const int row0 = tm * kNarrowM + wm * 64 + (lane >> 5) * 4;
-  const bool full = (tm + 1) * kNarrowM <= M && (tn + 1) * kNarrowN <= N;
-  store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
-    float v = acc[i][j][r];
-    if constexpr (V == kTermwise) {
-      v = __builtin_fmaf(xa[i][j][r], inv_s, v);
-      v = __builtin_fmaf(xb[i][j][r], inv_s, v);
+    // Wave w copies block w of A_hi and of A_lo (8 blocks each: two tiles of
+    // four) and block w of the eight blocks of B_hi and B_lo.
+    const uint16_t* src[3] = {
+        a_hi + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
+        a_lo + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
+        (w < 4 ? b_hi : b_lo) + tn * panel_stride + (w & 3) * 512 + lane * 8};
+    const int dst_off[3] = {kAH + w * 512, kAL + w * 512, (w < 4 ? kBH : kBL) + (w & 3) * 512};
+    const unsigned lds_base = lds_address(lds);
+    auto dma_one = [&](int kt, int n) {
+      const int ktc = min(kt, ktiles - 1);
+      dma16(src[n] + static_cast<int64_t>(ktc) * kTileHalves,
+            lds_base + ((kt % S) * kStageHalves + dst_off[n]) * 2);
+    };
+
+    const int fr = lane & 31, fk = lane >> 5;
+    int aoff[kSub], boff[kSub];
+  #pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+      aoff[i] = frag_offset(wm * 64 + i * 32 + fr, fk);
+      boff[i] = frag_offset(wn * 64 + i * 32 + fr, fk);
     }
-    return v;
-  });
+    auto rd = [&](int kt, int slot, int off) -> half8 {
+      return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + slot + off);
+    };
+    const floatx16 zero = {};
+    floatx16 acc[kSub][kSub], xa[kSub][kSub], xb[kSub][kSub];
+  #pragma unroll
+    for (int i = 0; i < kSub; ++i)
+  #pragma unroll
+      for (int j = 0; j < kSub; ++j) acc[i][j] = xa[i][j] = xb[i][j] = zero;
+    half8 ah[kSub], al[kSub], bh[kSub], bl[kSub];
+
+  #pragma unroll
+    for (int st = 0; st < S; ++st)
+  #pragma unroll
+      for (int n = 0; n < kDma; ++n) dma_one(st, n);
+    wait_vmcnt<(S - 1) * kDma>();
+    lds_barrier();
+  #pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+      ah[i] = rd(0, kAH, aoff[i]);
+      al[i] = rd(0, kAL, aoff[i]);
+      bh[i] = rd(0, kBH, boff[i]);
+      bl[i] = rd(0, kBL, boff[i]);
+    }
+
+    // One k-step: XA, then HH, then XB; each fragment is reloaded with step
+    // kt+1 once its last MFMA of the step is issued.  `first` marks the first
+    // step of an elementwise block (block sums restart), `last` its end (fold).
+    auto step = [&](int kt, bool first, bool last) {
+      const int nk = kt + 1;
+  #pragma unroll
+      for (int i = 0; i < kSub; ++i)
+  #pragma unroll
+        for (int j = 0; j < kSub; ++j)
+          xa[i][j] = mfma32(al[i], bh[j], (V == kElementwise && first) ? zero : xa[i][j]);
+      SCHED_FENCE();
+      wait_vmcnt<(S - 2) * kDma>();
+      lds_barrier();
+  #pragma unroll
+      for (int i = 0; i < kSub; ++i) al[i] = rd(nk, kAL, aoff[i]);
+      dma_one(kt + S, 0);
+      SCHED_FENCE();
+  #pragma unroll
+      for (int i = 0; i < kSub; ++i)
+  #pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
+      SCHED_FENCE();
+  #pragma unroll
+      for (int j = 0; j < kSub; ++j) bh[j] = rd(nk, kBH, boff[j]);
+      dma_one(kt + S, 1);
+      SCHED_FENCE();
+  #pragma unroll
+      for (int i = 0; i < kSub; ++i)
+  #pragma unroll
+        for (int j = 0; j < kSub; ++j)
+          xb[i][j] = mfma32(ah[i], bl[j], (V == kElementwise && first) ? zero : xb[i][j]);
+      SCHED_FENCE();
+  #pragma unroll
+      for (int i = 0; i < kSub; ++i) {
+        ah[i] = rd(nk, kAH, aoff[i]);
+        bl[i] = rd(nk, kBL, boff[i]);
+      }
+      dma_one(kt + S, 2);
+      SCHED_FENCE();
+      if constexpr (V == kElementwise) {
+        if (last) {
+          // End of block g: acc = (acc + XA_g / s) + XB_g / s.
+  #pragma unroll
+          for (int i = 0; i < kSub; ++i)
+  #pragma unroll
+            for (int j = 0; j < kSub; ++j)
+  #pragma unroll
+              for (int e = 0; e < 16; ++e) {
+                acc[i][j][e] = __builtin_fmaf(xa[i][j][e], inv_s, acc[i][j][e]);
+                acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
+              }
+        }
+      }
+    };
+    for (int kt = 0; kt < ktiles; kt += 2) {
+      step(kt, true, false);
+      step(kt + 1, false, true);
+    }
+    wait_vmcnt<0>();
+
+    const int col0 = tn * kNarrowN + wn * 64 + (lane & 31);
+    const int row0 = tm * kNarrowM + wm * 64 + (lane >> 5) * 4;
+    const bool full = (tm + 1) * kNarrowM <= M && (tn + 1) * kNarrowN <= N;
+    store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
+      float v = acc[i][j][r];
+      if constexpr (V == kTermwise) {
+        v = __builtin_fmaf(xa[i][j][r], inv_s, v);
+        v = __builtin_fmaf(xb[i][j][r], inv_s, v);
+      }
+      return v;
+    });
+  }
 }
 
 template <typename Kern>
@@ -507,7 +517,7 @@ hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
   const int tiles_m = static_cast<int>(p.Mp / kWide);
   const int tiles_n = static_cast<int>(p.Np / kWide);
   hipLaunchKernelGGL(gemm_wide_kernel<V>, dim3(tiles_m * tiles_n), dim3(kWideThreads), lds,
-                     stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range_flag,
+                     stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
                      static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
                      static_cast<int>(N), s, 1.0f / s);
   return hipGetLastError();
@@ -515,13 +525,17 @@ hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
 
 template <int V>
 hipError_t launch_narrow(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                         hipStream_t stream) {
+                         int cus, hipStream_t stream) {
   static const hipError_t attr = set_lds(&gemm_narrow_kernel<V>, kNarrowLdsBytes);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kNarrowM);
   const int tiles_n = static_cast<int>(p.Np / kNarrowN);
-  hipLaunchKernelGGL(gemm_narrow_kernel<V>, dim3(tiles_m * tiles_n), dim3(kNarrowThreads),
-                     kNarrowLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range_flag,
+  // One workgroup per compute unit (the kernel's occupancy), rounded to the
+  // 8 XCDs; fewer when there are fewer tiles.
+  const int grid = static_cast<int>(
+      std::min<int64_t>(static_cast<int64_t>(tiles_m) * tiles_n, std::max(8, cus / 8 * 8)));
+  hipLaunchKernelGGL(gemm_narrow_kernel<V>, dim3(grid), dim3(kNarrowThreads),
+                     kNarrowLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
                      static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
                      static_cast<int>(N), s, 1.0f / s);
   return hipGetLastError();
@@ -530,14 +544,14 @@ hipError_t launch_narrow(const Planes& p, int64_t M, int64_t N, float* C, int64_
 }  // namespace
 
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                       float scale, int variant, hipStream_t stream) {
+                       float scale, int variant, int cus, hipStream_t stream) {
   switch (variant) {
     case kElementwise: {
       const hipError_t e = launch_wide<kElementwise>(p, M, N, C, ldc, scale, stream);
       if (e != hipSuccess) return e;
-      return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, stream);
+      return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
     }
-    case kTermwise: return launch_narrow<kTermwise>(p, M, N, C, ldc, scale, stream);
+    case kTermwise: return launch_narrow<kTermwise>(p, M, N, C, ldc, scale, cus, stream);
     case kHiOnly: return launch_wide<kHiOnly>(p, M, N, C, ldc, scale, stream);
     default: return hipErrorInvalidValue;
   }

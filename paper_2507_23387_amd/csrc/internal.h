@@ -41,13 +41,14 @@ __host__ __device__ inline int64_t tiled_index(int64_t row, int64_t k, int64_t K
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-// Workspace: a header whose first int is the range flag, then the four
-// planes.  A planes are Mp x Kp, B planes Np x Kp (B transposed), all tiled.
-// range_flag != 0 after the split of B when some |B_hi| * s exceeds the
-// largest finite FP16 value (the scaled elementwise kernel cannot be used).
+// Workspace: a header holding the range flag, then the four planes.  A planes
+// are Mp x Kp, B planes Np x Kp (B transposed), all tiled.  The range flag is
+// two words: range[0] == range[1] after the split of B exactly when some
+// |B_hi| * s exceeds the largest finite FP16 value, so that the scaled
+// elementwise kernel cannot be used.
 struct Planes {
   int64_t Mp, Np, Kp;
-  int* range_flag;
+  uint32_t* range;
   uint16_t* a_hi;
   uint16_t* a_lo;
   uint16_t* b_hi;
@@ -70,12 +71,15 @@ hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A,
 
 // Enqueue the split of B (K x N row-major) into the tiled, transposed B
 // planes (Np x Kp), zero-filling the padding, and recompute the range flag.
+// `stamp` must differ from the stamp of the previous split into the same
+// workspace (the C-ABI draws a fresh one per call).
 hipError_t launch_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
-                          float scale, hipStream_t stream);
+                          float scale, uint32_t stamp, hipStream_t stream);
 
-// Enqueue the MFMA GEMM on prepared planes.
+// Enqueue the MFMA GEMM on prepared planes.  `cus` is the device's compute
+// unit count (sizes the persistent grid of the 256 x 128 kernel).
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                       float scale, int variant, hipStream_t stream);
+                       float scale, int variant, int cus, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).

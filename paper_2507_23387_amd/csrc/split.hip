@@ -69,19 +69,37 @@ __global__ __launch_bounds__(256) void split_rows_kernel(
   }
 }
 
-// Split of A into the tiled planes.  Thread = 8 consecutive k of one row (one
-// 16-byte chunk of each output plane); a workgroup covers 4 rows x 512 k, so
-// each wave reads 2 KiB of one row contiguously and the four rows of a
-// workgroup complete every 128-byte line they write.  blockIdx.y strides
-// over row quads.
+// 16-byte store that bypasses the caches' retention (the planes are streamed
+// out once and read back by the GEMM much later).
+__device__ __forceinline__ void store_stream(uint16_t* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
+__device__ __forceinline__ void split8(const float (&v)[8], float s, u32x4& hv, u32x4& lv) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint16_t h0, l0, h1, l1;
+    split_value(v[2 * e], s, h0, l0);
+    split_value(v[2 * e + 1], s, h1, l1);
+    hv[e] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+    lv[e] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+  }
+}
+
+// Split of A into the tiled planes.  A workgroup covers 16 rows x 128 k and a
+// wave 4 rows x 128 k: lane l takes 8 consecutive k of row l / 16, so each row
+// is read as one 512-byte piece, and the 16-byte chunks a store instruction
+// writes fill 8 whole 128-byte lines (4 rows x 32 bytes of one tile each).
+// blockIdx.y strides over row blocks.
 template <bool kVec>
 __global__ __launch_bounds__(256) void split_a_tiled_kernel(
     int64_t M, int64_t K, const float* __restrict__ X, int64_t ldx, uint16_t* __restrict__ hi,
     uint16_t* __restrict__ lo, int64_t Mp, int64_t Kp, float s) {
-  const int64_t k0 = (static_cast<int64_t>(blockIdx.x) * 64 + (threadIdx.x & 63)) * 8;
+  const int lane = threadIdx.x & 63;
+  const int64_t k0 = static_cast<int64_t>(blockIdx.x) * 128 + (lane & 15) * 8;
   if (k0 >= Kp) return;
-  for (int64_t m = static_cast<int64_t>(blockIdx.y) * 4 + (threadIdx.x >> 6); m < Mp;
-       m += static_cast<int64_t>(gridDim.y) * 4) {
+  for (int64_t m = static_cast<int64_t>(blockIdx.y) * 16 + (threadIdx.x >> 6) * 4 + (lane >> 4);
+       m < Mp; m += static_cast<int64_t>(gridDim.y) * 16) {
     float v[8];
     if (kVec && m < M && k0 + 7 < K) {
       const float4* src = reinterpret_cast<const float4*>(X + m * ldx + k0);
@@ -93,81 +111,77 @@ __global__ __launch_bounds__(256) void split_a_tiled_kernel(
       for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? X[m * ldx + k0 + e] : 0.0f;
     }
     u32x4 hv, lv;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      uint16_t h0, l0, h1, l1;
-      split_value(v[2 * e], s, h0, l0);
-      split_value(v[2 * e + 1], s, h1, l1);
-      hv[e] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-      lv[e] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
-    }
+    split8(v, s, hv, lv);
     const int64_t idx = tiled_index(m, k0, Kp);
-    *reinterpret_cast<u32x4*>(hi + idx) = hv;
-    *reinterpret_cast<u32x4*>(lo + idx) = lv;
+    store_stream(hi + idx, hv);
+    store_stream(lo + idx, lv);
   }
 }
 
 // Split of B (K x N row-major) into the tiled planes of B transposed.  One
-// workgroup = one 128 (n) x 16 (k) tile: thread t reads 8 consecutive n of
-// row k = t / 16 (each wave reads four 512-byte row pieces), the split values
-// are transposed through LDS, and thread t writes 16-byte chunk t of the 4 KiB
-// tile of each plane.  It also raises the range flag when some
-// |B_hi| * s > 65504 (the largest finite FP16 value).
+// workgroup = 32 k x 128 n (two tiles): thread t splits rows k and k+1
+// (k = 2 (t / 16)) at 8 consecutive n, each wave reading eight 512-byte row
+// pieces.  The (k, k+1) pairs of hi and of lo go to LDS as 32-bit words, n-major,
+// so each 16-byte chunk of a tile row is one LDS read; thread t then writes
+// chunk t of both tiles of both planes (4 KiB contiguous per tile).  It also
+// stamps the range flag (see launch_split_b) when some |B_hi| s > 65504, the
+// largest finite FP16 value.
 template <bool kVec>
 __global__ __launch_bounds__(256) void split_b_tiled_kernel(
     int64_t K, int64_t N, const float* __restrict__ B, int64_t ldb, uint16_t* __restrict__ hi,
-    uint16_t* __restrict__ lo, int64_t Kp, float s, int* __restrict__ range_flag) {
-  constexpr int kPitch = kSlice + 2;  // halves per LDS row: 36 bytes spread the banks
-  __shared__ uint16_t sh[kPanel * kPitch];
-  __shared__ uint16_t sl[kPanel * kPitch];
+    uint16_t* __restrict__ lo, int64_t Kp, float s, uint32_t* __restrict__ range, uint32_t stamp) {
+  constexpr int kK = 2 * kSlice;
+  constexpr int kPitch = kK / 2 + 4;  // words per n row; 16-byte aligned rows
+  __shared__ __align__(16) uint32_t ph[kPanel * kPitch];
+  __shared__ __align__(16) uint32_t pl[kPanel * kPitch];
   const int t = threadIdx.x;
-  const int64_t slice = blockIdx.x;
+  const int64_t kblock = blockIdx.x;
   const int64_t panel = blockIdx.y;
-  {
-    const int kl = t >> 4;
-    const int nl = (t & 15) * 8;
-    const int64_t k = slice * kSlice + kl;
-    const int64_t n = panel * kPanel + nl;
-    float v[8];
-    if (kVec && k < K && n + 7 < N) {
-      const float4* src = reinterpret_cast<const float4*>(B + k * ldb + n);
-      const float4 f0 = src[0], f1 = src[1];
-      v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
-      v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = (k < K && n + e < N) ? B[k * ldb + n + e] : 0.0f;
-    }
-    bool big = false;
+  const int nl = (t & 15) * 8;
+  const int kp = t >> 4;  // k pair
+  const int64_t k = kblock * kK + 2 * kp;
+  const int64_t n = panel * kPanel + nl;
+  float v0[8], v1[8];
+  if (kVec && k + 1 < K && n + 7 < N) {
+    const float4* r0 = reinterpret_cast<const float4*>(B + k * ldb + n);
+    const float4* r1 = reinterpret_cast<const float4*>(B + (k + 1) * ldb + n);
+    const float4 a0 = r0[0], a1 = r0[1], c0 = r1[0], c1 = r1[1];
+    v0[0] = a0.x; v0[1] = a0.y; v0[2] = a0.z; v0[3] = a0.w;
+    v0[4] = a1.x; v0[5] = a1.y; v0[6] = a1.z; v0[7] = a1.w;
+    v1[0] = c0.x; v1[1] = c0.y; v1[2] = c0.z; v1[3] = c0.w;
+    v1[4] = c1.x; v1[5] = c1.y; v1[6] = c1.z; v1[7] = c1.w;
+  } else {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      uint16_t h, l;
-      split_value(v[e], s, h, l);
-      big |= __builtin_fabsf(static_cast<float>(__builtin_bit_cast(_Float16, h))) * s > 65504.0f;
-      sh[(nl + e) * kPitch + kl] = h;
-      sl[(nl + e) * kPitch + kl] = l;
+      v0[e] = (k < K && n + e < N) ? B[k * ldb + n + e] : 0.0f;
+      v1[e] = (k + 1 < K && n + e < N) ? B[(k + 1) * ldb + n + e] : 0.0f;
     }
-    if (big) *range_flag = 1;
   }
-  __syncthreads();
-  {
-    const int r = t >> 1;
-    const int c = (t & 1) ^ tile_swizzle(r);  // logical chunk stored at position t & 1
-    const uint16_t* hrow = sh + r * kPitch + c * 8;
-    const uint16_t* lrow = sl + r * kPitch + c * 8;
-    u32x4 hv, lv;
+  bool big = false;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      hv[e] = static_cast<uint32_t>(hrow[2 * e]) | (static_cast<uint32_t>(hrow[2 * e + 1]) << 16);
-      lv[e] = static_cast<uint32_t>(lrow[2 * e]) | (static_cast<uint32_t>(lrow[2 * e + 1]) << 16);
-    }
-    const int64_t base = (panel * (Kp / kSlice) + slice) * kTileHalves + t * 8;
-    *reinterpret_cast<u32x4*>(hi + base) = hv;
-    *reinterpret_cast<u32x4*>(lo + base) = lv;
+  for (int e = 0; e < 8; ++e) {
+    uint16_t h0, l0, h1, l1;
+    split_value(v0[e], s, h0, l0);
+    split_value(v1[e], s, h1, l1);
+    big |= __builtin_fabsf(static_cast<float>(__builtin_bit_cast(_Float16, h0))) * s > 65504.0f;
+    big |= __builtin_fabsf(static_cast<float>(__builtin_bit_cast(_Float16, h1))) * s > 65504.0f;
+    ph[(nl + e) * kPitch + kp] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+    pl[(nl + e) * kPitch + kp] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+  }
+  if (big) range[0] = stamp;
+  if (t == 0) range[1] = stamp;
+  __syncthreads();
+  const int r = t >> 1;
+  const int c = (t & 1) ^ tile_swizzle(r);  // logical chunk stored at position t & 1
+#pragma unroll
+  for (int sl = 0; sl < kK / kSlice; ++sl) {
+    const u32x4 hv = *reinterpret_cast<const u32x4*>(ph + r * kPitch + sl * 8 + c * 4);
+    const u32x4 lv = *reinterpret_cast<const u32x4*>(pl + r * kPitch + sl * 8 + c * 4);
+    const int64_t base = (panel * (Kp / kSlice) + kblock * (kK / kSlice) + sl) * kTileHalves + t * 8;
+    store_stream(hi + base, hv);
+    store_stream(lo + base, lv);
   }
 }
-
-__global__ void flag_reset_kernel(int* range_flag) { *range_flag = 0; }
 
 __global__ __launch_bounds__(256) void zero_kernel(int64_t M, int64_t N, float* __restrict__ C,
                                                    int64_t ldc) {
@@ -203,7 +217,7 @@ hipError_t launch_split_rows(int64_t rows, int64_t cols, const float* X, int64_t
 hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
                           float scale, hipStream_t stream) {
   // Mp is a multiple of 256 and Kp of 64 (plan_planes).
-  const dim3 grid(static_cast<unsigned>((p.Kp + 511) / 512), grid_rows(p.Mp / 4));
+  const dim3 grid(static_cast<unsigned>((p.Kp + 127) / 128), grid_rows(p.Mp / 16));
   const bool vec = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (lda % 4 == 0);
   if (vec)
     hipLaunchKernelGGL(split_a_tiled_kernel<true>, grid, dim3(256), 0, stream, M, K, A, lda,
@@ -215,20 +229,20 @@ hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A,
 }
 
 hipError_t launch_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
-                          float scale, hipStream_t stream) {
-  hipLaunchKernelGGL(flag_reset_kernel, dim3(1), dim3(1), 0, stream, p.range_flag);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // One workgroup per tile: Kp / 16 slices x Np / 128 panels (Np / 128 <= 65535
-  // is checked by the C-ABI).
-  const dim3 grid(static_cast<unsigned>(p.Kp / kSlice), static_cast<unsigned>(p.Np / kPanel));
+                          float scale, uint32_t stamp, hipStream_t stream) {
+  // One workgroup per two tiles: Kp / 32 k blocks x Np / 128 panels (Np / 128
+  // <= 65535 is checked by the C-ABI).  Every workgroup writes range[1] =
+  // stamp and the ones that see an FP16 overflow of s B_hi write range[0] =
+  // stamp, so range[0] == range[1] afterwards exactly when this split found
+  // one; a fresh stamp per call makes a reset pass unnecessary.
+  const dim3 grid(static_cast<unsigned>(p.Kp / (2 * kSlice)), static_cast<unsigned>(p.Np / kPanel));
   const bool vec = (reinterpret_cast<uintptr_t>(B) % 16 == 0) && (ldb % 4 == 0);
   if (vec)
     hipLaunchKernelGGL(split_b_tiled_kernel<true>, grid, dim3(256), 0, stream, K, N, B, ldb,
-                       p.b_hi, p.b_lo, p.Kp, scale, p.range_flag);
+                       p.b_hi, p.b_lo, p.Kp, scale, p.range, stamp);
   else
     hipLaunchKernelGGL(split_b_tiled_kernel<false>, grid, dim3(256), 0, stream, K, N, B, ldb,
-                       p.b_hi, p.b_lo, p.Kp, scale, p.range_flag);
+                       p.b_hi, p.b_lo, p.Kp, scale, p.range, stamp);
   return hipGetLastError();
 }
 

@@ -151,10 +151,12 @@ def test_elementwise_range_switch(gpu, edge):
 
 
 def _range_flag(ws):
-    """The range flag is the first int of the workspace header."""
+    """The workspace header starts with two stamp words; they are equal after a
+    split of B that found |B_hi| s > 65504."""
     import torch
 
-    return int(ws[:4].view(torch.int32).item())
+    w = ws[:8].view(torch.int32).cpu()
+    return int(w[0] == w[1])
 
 
 def test_range_flag_follows_the_last_split_of_b(gpu):
