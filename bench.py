@@ -41,7 +41,8 @@ THREE_GEMM_PEAK_TFLOPS = FP16_PEAK_TFLOPS / 3
 HBM_PEAK_GBS = 8000.0
 # The MFMA kernel that runs for each order (the elementwise call also launches
 # the narrow kernel, which reads the range flag and returns at once).
-GEMM_KERNELS = {"elementwise": "gemm_wide_kernel<0>", "termwise": "gemm_narrow_kernel<1>"}
+GEMM_KERNELS = {"elementwise": "gemm_wide_kernel<0>", "termwise": "gemm_narrow_kernel<1>",
+                "elementwise_cross_first": "gemm_narrow_kernel<3>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
@@ -129,7 +130,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c3")
-    ap.add_argument("--order", default=None, help="elementwise | termwise")
+    ap.add_argument("--order", default=None, help="elementwise | termwise | elementwise_cross_first")
     ap.add_argument("--scale", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)

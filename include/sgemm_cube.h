@@ -49,8 +49,12 @@ extern "C" {
 
 /* Accumulation orders (Sec. 4.5). */
 typedef enum {
-  SGEMM_CUBE_ELEMENTWISE = 0, /* Eq. elementwise */
-  SGEMM_CUBE_TERMWISE = 1     /* Eq. termwise */
+  SGEMM_CUBE_ELEMENTWISE = 0,             /* Eq. elementwise */
+  SGEMM_CUBE_TERMWISE = 1,                /* Eq. termwise */
+  SGEMM_CUBE_ELEMENTWISE_CROSS_FIRST = 2  /* the reordering proposed at the end of
+                                             Sec. 4.5: per block g,
+                                             acc = acc + ((XA_g + XB_g) / s + HH_g),
+                                             blocks of 2 * sgemm_cube_block_k() */
 } sgemm_cube_order_t;
 
 /* Status codes returned by every entry point. */
@@ -75,7 +79,8 @@ typedef enum {
  *                valid range for an input's exponent window; 2^11 is the fixed
  *                choice valid over the whole normal-FP16 range.  Any other
  *                value -> SGEMM_CUBE_ERR_INVALID_VALUE.
- *   accum_order  SGEMM_CUBE_ELEMENTWISE or SGEMM_CUBE_TERMWISE.
+ *   accum_order  SGEMM_CUBE_ELEMENTWISE, SGEMM_CUBE_TERMWISE or
+ *                SGEMM_CUBE_ELEMENTWISE_CROSS_FIRST.
  *   stream       HIP stream the work is enqueued on.
  *
  * Needs device workspace of sgemm_cube_workspace_size(M, N, K, accum_order)

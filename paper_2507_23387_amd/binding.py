@@ -18,7 +18,9 @@ LIB_PATH = os.path.join(_HERE, "libsgemmcube.so")
 
 ELEMENTWISE = 0
 TERMWISE = 1
-ORDERS = {"elementwise": ELEMENTWISE, "termwise": TERMWISE}
+ELEMENTWISE_CROSS_FIRST = 2
+ORDERS = {"elementwise": ELEMENTWISE, "termwise": TERMWISE,
+          "elementwise_cross_first": ELEMENTWISE_CROSS_FIRST}
 
 STATUS_OK = 0
 STATUS_NAMES = {

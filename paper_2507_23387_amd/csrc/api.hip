@@ -35,6 +35,20 @@ namespace {
 // every grid dimension within its hardware limit.
 constexpr int64_t kMaxDim = (int64_t{1} << 30);
 
+bool valid_order(int order) {
+  return order == SGEMM_CUBE_ELEMENTWISE || order == SGEMM_CUBE_TERMWISE ||
+         order == SGEMM_CUBE_ELEMENTWISE_CROSS_FIRST;
+}
+
+// Public accumulation order -> internal kernel variant.
+int variant_of(int order) {
+  switch (order) {
+    case SGEMM_CUBE_ELEMENTWISE: return kElementwise;
+    case SGEMM_CUBE_TERMWISE: return kTermwise;
+    default: return kCrossFirst;
+  }
+}
+
 bool valid_scale(float s) {
   if (!std::isfinite(s) || s < 1.0f || s > 16777216.0f) return false;
   int e = 0;
@@ -183,18 +197,17 @@ extern "C" {
 int sgemm_cube(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
                int64_t ldb, float* C, int64_t ldc, float scale, int accum_order,
                hipStream_t stream) {
-  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE)
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
   const int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
   if (st != SGEMM_CUBE_OK) return st;
-  return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, stream);
+  return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, scale,
+                             sgc::variant_of(accum_order), stream);
 }
 
 int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
                   int64_t ldb, float* C, int64_t ldc, float scale, int accum_order, void* ws,
                   size_t ws_bytes, hipStream_t stream) {
-  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE)
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
   int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
   if (st != SGEMM_CUBE_OK) return st;
   const size_t need = sgc::ws_size(M, N, K);
@@ -206,7 +219,8 @@ int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
         sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
       return SGEMM_CUBE_ERR_INVALID_VALUE;
   }
-  return sgc::run(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, ws, stream);
+  return sgc::run(M, N, K, A, lda, B, ldb, C, ldc, scale, sgc::variant_of(accum_order), ws,
+                  stream);
 }
 
 int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
@@ -235,8 +249,7 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 
 int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
                        int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE)
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !sgc::valid_scale(scale))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
@@ -252,14 +265,15 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
   if (sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   const sgc::Planes p = sgc::plan_planes(M, N, K, const_cast<void*>(ws));
-  return sgc::launch_gemm(p, M, N, C, ldc, scale, accum_order, sgc::current_cus(), stream) ==
+  return sgc::launch_gemm(p, M, N, C, ldc, scale, sgc::variant_of(accum_order),
+                         sgc::current_cus(), stream) ==
                  hipSuccess
              ? SGEMM_CUBE_OK
              : SGEMM_CUBE_ERR_HIP;
 }
 
 size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order) {
-  if (accum_order != SGEMM_CUBE_ELEMENTWISE && accum_order != SGEMM_CUBE_TERMWISE) return 0;
+  if (!sgc::valid_order(accum_order)) return 0;
   if (M < 0 || N < 0 || K < 0 || M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim)
     return 0;
   return sgc::ws_size(M, N, K);

@@ -26,6 +26,10 @@
 // gemm_narrow_kernel, 256 x 128 tiles, 8 waves of 64 x 64 (two per SIMD):
 //   kTermwise (Eq. termwise): three FP32 accumulators over all of K,
 //     C = (HH + XA / s) + XB / s in the epilogue.
+//   kCrossFirst (the reordered elementwise accumulation proposed at the end
+//     of Sec. 4.5): per block g of two k-steps the cross products are summed
+//     first, X_g = XA_g + XB_g (one MFMA chain), HH_g separately, and
+//     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
 //   kElementwise when the range flag is set: unscaled, blocks of two k-steps
 //     (32): HH goes straight into the accumulator, XA_g and XB_g into block
 //     sums started from zero, and acc = (acc + XA_g / s) + XB_g / s with two
@@ -355,7 +359,7 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
-  static_assert(V == kElementwise || V == kTermwise, "narrow kernel variants");
+  static_assert(V == kElementwise || V == kTermwise || V == kCrossFirst, "narrow kernel variants");
   constexpr int S = kNarrowStages;
   constexpr int kAHalves = kNarrowM * kSlice;  // A plane slot: two tiles
   constexpr int kBHalves = kNarrowN * kSlice;  // B plane slot: one tile
@@ -429,37 +433,50 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
 
     // One k-step: XA, then HH, then XB; each fragment is reloaded with step
     // kt+1 once its last MFMA of the step is issued.  `first` marks the first
-    // step of an elementwise block (block sums restart), `last` its end (fold).
+    // step of a block (block sums restart), `last` its end (fold).  Register
+    // sets: termwise acc = HH, xa = XA, xb = XB; elementwise fallback acc =
+    // running sum, xa = XA_g, xb = XB_g; cross-first acc = running sum, xa =
+    // X_g = XA_g + XB_g, xb = HH_g.
+    constexpr bool kBlocks = V != kTermwise;
     auto step = [&](int kt, bool first, bool last) {
       const int nk = kt + 1;
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < kSub; ++i)
-  #pragma unroll
+#pragma unroll
         for (int j = 0; j < kSub; ++j)
-          xa[i][j] = mfma32(al[i], bh[j], (V == kElementwise && first) ? zero : xa[i][j]);
+          xa[i][j] = mfma32(al[i], bh[j], (kBlocks && first) ? zero : xa[i][j]);
       SCHED_FENCE();
       wait_vmcnt<(S - 2) * kDma>();
       lds_barrier();
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < kSub; ++i) al[i] = rd(nk, kAL, aoff[i]);
       dma_one(kt + S, 0);
       SCHED_FENCE();
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < kSub; ++i)
-  #pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) {
+          if constexpr (V == kCrossFirst)
+            xb[i][j] = mfma32(ah[i], bh[j], first ? zero : xb[i][j]);
+          else
+            acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
+        }
       SCHED_FENCE();
-  #pragma unroll
+#pragma unroll
       for (int j = 0; j < kSub; ++j) bh[j] = rd(nk, kBH, boff[j]);
       dma_one(kt + S, 1);
       SCHED_FENCE();
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < kSub; ++i)
-  #pragma unroll
-        for (int j = 0; j < kSub; ++j)
-          xb[i][j] = mfma32(ah[i], bl[j], (V == kElementwise && first) ? zero : xb[i][j]);
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) {
+          if constexpr (V == kCrossFirst)
+            xa[i][j] = mfma32(ah[i], bl[j], xa[i][j]);
+          else
+            xb[i][j] = mfma32(ah[i], bl[j], (kBlocks && first) ? zero : xb[i][j]);
+        }
       SCHED_FENCE();
-  #pragma unroll
+#pragma unroll
       for (int i = 0; i < kSub; ++i) {
         ah[i] = rd(nk, kAH, aoff[i]);
         bl[i] = rd(nk, kBL, boff[i]);
@@ -469,15 +486,26 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
       if constexpr (V == kElementwise) {
         if (last) {
           // End of block g: acc = (acc + XA_g / s) + XB_g / s.
-  #pragma unroll
+#pragma unroll
           for (int i = 0; i < kSub; ++i)
-  #pragma unroll
+#pragma unroll
             for (int j = 0; j < kSub; ++j)
-  #pragma unroll
+#pragma unroll
               for (int e = 0; e < 16; ++e) {
                 acc[i][j][e] = __builtin_fmaf(xa[i][j][e], inv_s, acc[i][j][e]);
                 acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
               }
+        }
+      } else if constexpr (V == kCrossFirst) {
+        if (last) {
+          // End of block g: acc = acc + (X_g / s + HH_g).
+#pragma unroll
+          for (int i = 0; i < kSub; ++i)
+#pragma unroll
+            for (int j = 0; j < kSub; ++j)
+#pragma unroll
+              for (int e = 0; e < 16; ++e)
+                acc[i][j][e] += __builtin_fmaf(xa[i][j][e], inv_s, xb[i][j][e]);
         }
       }
     };
@@ -552,6 +580,7 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
       return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
     }
     case kTermwise: return launch_narrow<kTermwise>(p, M, N, C, ldc, scale, cus, stream);
+    case kCrossFirst: return launch_narrow<kCrossFirst>(p, M, N, C, ldc, scale, cus, stream);
     case kHiOnly: return launch_wide<kHiOnly>(p, M, N, C, ldc, scale, stream);
     default: return hipErrorInvalidValue;
   }

@@ -9,9 +9,9 @@
 
 namespace sgc {
 
-// Internal accumulation variants: the two public orders plus the
-// high-high-only baseline.
-enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2 };
+// Internal accumulation variants: the public orders plus the high-high-only
+// baseline.
+enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2, kCrossFirst = 3 };
 
 // Plane layout in the workspace ("panel tiles").  Every FP16 plane (A_hi,
 // A_lo, and B_hi, B_lo of B transposed) is cut into panels of kPanel rows and
@@ -85,8 +85,9 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);
 
-// The elementwise k-block of the scaled kernel (one MFMA k-step) and of the
-// fallback kernel used when the range flag is set.
+// The elementwise k-block of the scaled kernel (one MFMA k-step), and of the
+// fallback kernel used when the range flag is set and of the cross-terms-first
+// order (two k-steps).
 constexpr int kBlockScaled = kSlice;
 constexpr int kBlockFallback = 2 * kSlice;
 

@@ -79,7 +79,7 @@ def call(lib, M=4, N=4, K=4, A=FAKE, lda=None, B=FAKE + (1 << 30), ldb=None,
     dict(A=0), dict(B=0), dict(C=0),
     dict(scale=3.0), dict(scale=0.5), dict(scale=2.0**25), dict(scale=float("inf")),
     dict(scale=float("nan")), dict(scale=-2048.0), dict(scale=0.0),
-    dict(order=2), dict(order=-1),
+    dict(order=3), dict(order=-1),
     dict(C=FAKE + 8),                        # C overlaps A
     dict(C=FAKE + (1 << 30) + 4),            # C overlaps B
 ])
@@ -96,6 +96,12 @@ def test_valid_scales_accepted_by_validation(lib):
     # returns before any device work.
     for s_b in (0, 1, 11, 12, 13, 24):
         assert call(lib, M=0, scale=2.0**s_b) == 0
+
+
+def test_all_orders_accepted_by_validation(lib):
+    for order in (0, 1, 2):
+        assert call(lib, M=0, order=order) == 0
+        assert lib.sgemm_cube_workspace_size(5, 5, 5, order) > 0
 
 
 def test_degenerate_shapes_are_noops(lib):

@@ -21,17 +21,20 @@ from tests.helpers import abs_ab, assert_parity, ref64
 
 pytestmark = pytest.mark.gpu
 
-ORDERS = ["elementwise", "termwise"]
+ORDERS = ["elementwise", "termwise", "elementwise_cross_first"]
 SHAPES = [
     (1, 1, 1), (1, 7, 3), (5, 3, 1), (17, 33, 65), (64, 64, 64), (128, 128, 64),
     (129, 130, 65), (300, 200, 1000), (256, 256, 256), (200, 129, 4103), (513, 640, 192),
 ]
 
 
-def _kb():
+def _kb(order="elementwise"):
+    """The oracle's block size matching the GPU's: one MFMA k-step, two for the
+    cross-terms-first order."""
     from paper_2507_23387_amd import binding
 
-    return binding.sgemm_cube_block_k()
+    kb = binding.sgemm_cube_block_k()
+    return 2 * kb if order == "elementwise_cross_first" else kb
 
 
 @pytest.mark.parametrize("order", ORDERS)
@@ -41,7 +44,7 @@ def test_shapes_full_parity(gpu, order, shape):
     log(f"gemm {order} {M}x{N}x{K}")
     A, B = workloads.make_operands(M, N, K, M + N + K, "normal")
     C = gemm(A, B, 2048.0, order)
-    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb())
+    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb(order))
     assert_parity(C, Co, K, abs_ab(A, B), f"{order} {shape}")
 
 
@@ -77,7 +80,7 @@ def test_padded_leading_dimensions_and_misaligned_bases(gpu, order):
     Cn = Cv.cpu().numpy()
     assert np.isnan(Cn[:, N:]).all(), "wrote outside the M x N block"
     assert np.isnan(Cbuf[:2].cpu().numpy()).all()
-    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb())
+    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb(order))
     assert_parity(Cn[:, :N], Co, K, abs_ab(A, B), "padded")
 
 
@@ -115,7 +118,7 @@ def test_non_finite_inputs_propagate_like_the_oracle(gpu, order):
     B[20, 21] = 32784.0    # lo overflows with s = 2^12 (Sec. 4.2 example)
     log(f"gemm non-finite {order}")
     C = gemm(A, B, 4096.0, order)
-    Co = oracle.sgemm(A, B, 4096.0, order, kb=_kb())
+    Co = oracle.sgemm(A, B, 4096.0, order, kb=_kb(order))
     assert_parity(C, Co, K, abs_ab(A, B), "non-finite")
     assert np.isnan(Co).any()
 
@@ -310,6 +313,8 @@ CASES = [
     ("c4", "elementwise", 2.0**11), ("c4", "termwise", 2.0**11),
     ("c5", "termwise", 2.0**11), ("c5", "termwise", 2.0**13),
     ("c5", "elementwise", 2.0**11), ("c5", "elementwise", 2.0**13),
+    ("c2", "elementwise_cross_first", 2.0**11), ("c4", "elementwise_cross_first", 2.0**11),
+    ("c5", "elementwise_cross_first", 2.0**13),
 ]
 _CACHE = {}
 
@@ -330,7 +335,7 @@ def test_workload_parity_sampled_rows(gpu, name, order, scale):
     C = gemm(A, B, scale, order)
     assert C.shape == (w.M, w.N)
     rows = np.arange(w.M) if w.M <= 256 else workloads.sample_rows(w.M, 16, w.seed)
-    Co = oracle.sgemm_rows(A, B, rows, scale, order, kb=_kb())
+    Co = oracle.sgemm_rows(A, B, rows, scale, order, kb=_kb(order))
     absab = abs_ab(A, B, rows)
     assert_parity(C[rows], Co, w.K, absab, f"{name} {order}")
     # The whole output is finite (every workload stays in range).
