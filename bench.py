@@ -132,6 +132,8 @@ def main():
     ap.add_argument("--workload", default="c3")
     ap.add_argument("--order", default=None, help="elementwise | termwise | elementwise_cross_first")
     ap.add_argument("--scale", type=float, default=None)
+    ap.add_argument("--prescale", action="store_true",
+                    help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-errors", action="store_true")
@@ -161,7 +163,8 @@ def main():
     dA = torch.from_numpy(A).to(dev)
     dB = torch.from_numpy(B).to(dev)
     dC = torch.empty((M, N), dtype=torch.float32, device=dev)
-    ws_bytes = sgc.sgemm_cube_workspace_size(M, N, K, order_code)
+    ws_bytes = (sgc.sgemm_cube_ex_workspace_size(M, N, K, order_code, sgc.binding.OPT_PRESCALE)
+                if args.prescale else sgc.sgemm_cube_workspace_size(M, N, K, order_code))
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
@@ -177,6 +180,19 @@ def main():
                                     ws_bytes, sh)
         if st:
             raise sgc.SgemmCubeError(st, "sgemm_cube_compute")
+
+    if args.prescale:
+        # The pre-scaled call has no split/compute halves: the whole call is
+        # timed in the "compute" slot and the "prepare" slot is empty.
+        def prepare():
+            pass
+
+        def compute():
+            st = sgc.sgemm_cube_ex(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, dC.data_ptr(), N,
+                                   scale, order_code, sgc.binding.OPT_PRESCALE, ws.data_ptr(),
+                                   ws_bytes, None, sh)
+            if st:
+                raise sgc.SgemmCubeError(st, "sgemm_cube_ex")
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
@@ -270,7 +286,8 @@ def main():
         "dtype": "f16 MFMA products, f32 accumulation (f32 in/out)",
         "data": "synthetic",
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "seed": w.seed,
-                   "distribution": w.dist, "scale": scale, "order": order},
+                   "distribution": w.dist, "scale": scale, "order": order,
+                   **({"prescale": True} if args.prescale else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,
         **extra,

@@ -10,7 +10,10 @@ Runs the experiments of Sec. 6.1-6.2 on this GPU with synthetic inputs:
   mkn      error vs m = n = k;
   maxnorm  componentwise errors on adversarial inputs (the max-norm study the
            paper leaves open): max |C - C64| / (|A||B|) and the largest
-           relative error over nonzero entries.
+           relative error over nonzero entries;
+  prescale the offset sweep's low and high exponents again with the
+           power-of-two pre-scaling of sgemm_cube_ex, which keeps hi normal
+           and in range.
 
 Compared: the three GPU accumulation orders, the GPU FP16 baseline
 (sgemm_cube_hgemm), and the host's FP32 SGEMM (numpy float32 matmul; numpy's
@@ -56,6 +59,15 @@ class Runner:
         self.torch, self.sgc = torch, sgc
         self.dev = torch.device("cuda:0")
 
+    def prescaled(self, A, B, s_b):
+        torch, sgc = self.torch, self.sgc
+        dA = torch.from_numpy(A).to(self.dev)
+        dB = torch.from_numpy(B).to(self.dev)
+        out = {f"{order}/{s_b}/pre": sgc.matmul_ex(dA, dB, scale=2.0**s_b, order=order,
+                                                  prescale=True) for order in ORDERS}
+        torch.cuda.synchronize()
+        return {k: v.cpu().numpy() for k, v in out.items()}
+
     def methods(self, A, B, scales):
         torch, sgc = self.torch, self.sgc
         dA = torch.from_numpy(A).to(self.dev)
@@ -87,6 +99,27 @@ def offset_sweep(run, n, exps, seeds, out):
                 f"elementwise/12 {row['elementwise/12']:.3g} sgemm {row['sgemm_fp32_host']:.3g} "
                 f"hgemm {row['hgemm']:.3g}")
     out["offset"] = {"n": n, "seeds": list(seeds), "rows": rows}
+
+
+def prescale_sweep(run, n, exps, seeds, out):
+    rows = []
+    for sym in (True, False):
+        for e in exps:
+            acc = {}
+            for seed in seeds:
+                A, B = workloads.offset_exponent_operands(n, n, n, seed, e, symmetric=sym)
+                ref = A.astype(np.float64) @ B.astype(np.float64)
+                res = run.prescaled(A, B, 11)
+                res.update({k: v for k, v in run.methods(A, B, (11,)).items()
+                            if k in ("termwise/11", "elementwise/11", "sgemm_fp32_host")})
+                for k, C in res.items():
+                    acc.setdefault(k, []).append(frob(C, ref))
+            row = {"dist": "symmetric" if sym else "nonnegative", "e": e,
+                   **{k: float(np.mean(v)) for k, v in acc.items()}}
+            rows.append(row)
+            log(f"prescale {row['dist']} e={e}: termwise {row['termwise/11']:.3g} -> "
+                f"{row['termwise/11/pre']:.3g}")
+    out["prescale"] = {"n": n, "seeds": list(seeds), "rows": rows}
 
 
 def size_sweep(run, name, shapes, seeds, out):
@@ -211,6 +244,16 @@ def to_markdown(res) -> str:
                      r["elementwise_cross_first/12"]]
             lines.append(f"| {r['m']} | {r['n']} | {r['k']} | " + " | ".join(fmt(c) for c in cells) + " |")
         lines.append("")
+    pre = res["prescale"]
+    lines += [f"## Pre-scaled (sgemm_cube_ex, PRESCALE), s = 2^11, m = n = k = {pre['n']}, "
+              f"seeds {pre['seeds']}", "",
+              "| dist | e | sgemm | ew | ew pre | tw | tw pre | cf pre |",
+              "|---|---|---|---|---|---|---|---|"]
+    for r in pre["rows"]:
+        cells = [r["sgemm_fp32_host"], r["elementwise/11"], r["elementwise/11/pre"],
+                 r["termwise/11"], r["termwise/11/pre"], r["elementwise_cross_first/11/pre"]]
+        lines.append(f"| {r['dist']} | {r['e']} | " + " | ".join(fmt(c) for c in cells) + " |")
+    lines.append("")
     mx = res["maxnorm"]
     lines += [f"## Max-norm errors on adversarial inputs (M = {mx['M']}, N = {mx['N']}, K = {mx['K']}, "
               f"s = 2^11, worst over seeds {mx['seeds']})", "",
@@ -250,12 +293,14 @@ def main():
         size_sweep(run, "k", [(256, 256, 256), (256, 256, 4096)], (0,), res)
         size_sweep(run, "mkn", [(256, 256, 256), (512, 512, 512)], (0,), res)
         maxnorm_study(run, 128, 128, 1024, (0,), res)
+        prescale_sweep(run, 256, (-24, 0, 20), (0,), res)
     else:
         offset_sweep(run, 1024, tuple(range(-20, 13, 2)), (0, 1, 2, 3, 4), res)
         size_sweep(run, "mn", [(n, n, 2816) for n in (256, 512, 1024, 2048, 4096, 8192)], (0, 1, 2), res)
         size_sweep(run, "k", [(1024, 1024, k) for k in (256, 1024, 4096, 16384, 65536)], (0, 1, 2), res)
         size_sweep(run, "mkn", [(n, n, n) for n in (512, 1024, 2048, 4096)], (0, 1, 2), res)
         maxnorm_study(run, 512, 512, 8192, (0, 1, 2), res)
+        prescale_sweep(run, 1024, (-28, -24, -20, -16, 0, 16, 20, 24), (0, 1, 2, 3, 4), res)
     res["seconds"] = time.perf_counter() - t0
     if args.out:
         with open(args.out, "w") as f:

@@ -103,6 +103,55 @@ int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
                   int64_t ldb, float* C, int64_t ldc, float scale, int accum_order, void* ws,
                   size_t ws_bytes, hipStream_t stream);
 
+/* Options of sgemm_cube_ex (bit mask). */
+enum { SGEMM_CUBE_OPT_PRESCALE = 1 };
+
+/* Range classes reported by sgemm_cube_ex (bit mask; Sec. 3.1 and 4.2). */
+enum {
+  SGEMM_CUBE_RANGE_NONFINITE = 1,    /* an input entry is inf or NaN */
+  SGEMM_CUBE_RANGE_HI_OVERFLOW = 2,  /* a finite entry has |a| >= 65520: fl16(a) is infinite */
+  SGEMM_CUBE_RANGE_LO_OVERFLOW = 4,  /* a scaled residual overflowed FP16 (Rule 2 violated) */
+  SGEMM_CUBE_RANGE_HI_SUBNORMAL = 8  /* a nonzero hi is FP16-subnormal: the 22-bit guarantee
+                                        of Sec. 4.2 does not hold for that entry */
+};
+
+/*
+ * sgemm_cube_ws with the range extensions that Sec. 4.2 leaves out of scope
+ * and Sec. 7 and 8 name as the way to widen the method's range (explicit
+ * exponent management of the high part, input-dependent scaling, an overflow
+ * guard):
+ *   options      0 or SGEMM_CUBE_OPT_PRESCALE.  With PRESCALE, row i of A is
+ *                multiplied by 2^p_i and column j of B by 2^q_j before the
+ *                split, powers of two that bring the row's (column's) largest
+ *                finite magnitude into [2^EA, 2^(EA+1)) with
+ *                EA = min(14, 26 - s_b) (columns: [2^EB, 2^(EB+1)),
+ *                EB = 14 - s_b, for scale = 2^s_b); the three-product GEMM
+ *                runs on the scaled operands and C_ij = 2^-(p_i + q_j) C'_ij.
+ *                The scaling is exact, so entries whose hi would be subnormal
+ *                or would overflow FP16 are brought into the normal range as
+ *                long as they are within ~28 (A) / ~17 (B, s = 2^11) binades
+ *                of their row's (column's) largest entry.  A row (column) with
+ *                no nonzero finite entry is left unscaled.  Costs one extra
+ *                read of A and B and one read-write of C.
+ *   range_report NULL, or a 4-byte-aligned DEVICE pointer to one uint32 that
+ *                receives, in stream order, the OR of the SGEMM_CUBE_RANGE_*
+ *                classes found among the (pre-scaled) entries of A and B; 0 when
+ *                M, N or K is 0.  Must not overlap A, B, C or the workspace.
+ *   ws, ws_bytes at least sgemm_cube_ex_workspace_size(M, N, K, accum_order,
+ *                options) bytes, 256-byte aligned; otherwise as sgemm_cube_ws.
+ * Other arguments and errors as sgemm_cube_ws; unknown option bits ->
+ * SGEMM_CUBE_ERR_INVALID_VALUE.
+ */
+int sgemm_cube_ex(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                  int64_t ldb, float* C, int64_t ldc, float scale, int accum_order,
+                  unsigned options, void* ws, size_t ws_bytes, uint32_t* range_report,
+                  hipStream_t stream);
+
+/* Workspace bytes sgemm_cube_ex needs (0 for degenerate shapes or invalid
+ * arguments). */
+size_t sgemm_cube_ex_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order,
+                                    unsigned options);
+
 /*
  * Two-phase form of sgemm_cube_ws, for callers that reuse a split operand
  * (for example a constant B) or time the two passes separately:

@@ -21,6 +21,18 @@ Functions and what pins them (see tests/test_oracle_*.py):
   (FP16-exact inputs, one block).  ELEMENTWISE_CROSS_FIRST has no printed
   bound; beyond the shared truncation and a derived summation bound its
   parity is unpinned.
+* ``prescale_exponents`` / ``sgemm_prescaled`` / ``range_classes``: the
+  range extensions the paper names without fixing a rule (exponent
+  management of the high part, Sec. 4.2; input-dependent scaling and an
+  overflow guard, Sec. 7 and 8), in this reading: each row of A (column of B)
+  is multiplied by the power of two that brings its largest finite magnitude
+  to [2^EA, 2^(EA+1)), EA = min(14, 26 - s_b) (B: EB = 14 - s_b), the method
+  runs on the scaled operands, and C_ij is scaled back by 2^-(p_i + q_j).
+  Pinned by exact invariance (inputs whose hi and lo stay normal give the
+  unscaled result bit for bit), by Eq. main_bound holding after pre-scaling
+  on inputs whose hi is FP16-subnormal, and by the range classes of the
+  values Sec. 3.1 and Sec. 4.2 name (|a| >= 65520, the 32784 residual
+  overflow at s_b = 12, subnormal hi).
 * ``bounds``: exact-rational bound calculators (Eq. ll_bound,
   Eq. truncation, Eq. main_bound) and the residual-class probability model of
   Sec. 4.1, pinned by the statements the paper prints about them.
@@ -156,3 +168,65 @@ def sgemm_rows(A, B, rows, scale: float, order="elementwise", kb: int = DEFAULT_
     own row of A and all of B, so this is the full-size result sampled."""
     rows = np.asarray(rows, dtype=np.int64)
     return sgemm(np.asarray(A)[rows], B, scale, order, kb, threads)
+
+
+def prescale_exponents(X, axis: int, target: int) -> np.ndarray:
+    """Power-of-two exponents that bring the largest finite |X| of every row
+    (axis=1) or column (axis=0) into [2^target, 2^(target+1)); 0 where the
+    line has no nonzero finite entry."""
+    X = np.abs(np.asarray(X, dtype=np.float64))
+    X = np.where(np.isfinite(X), X, 0.0)
+    m = X.max(axis=axis) if X.size else np.zeros(X.shape[1 - axis])
+    _, e = np.frexp(m)          # m = f 2^e with f in [0.5, 1): floor(log2 m) = e - 1
+    return np.where(m > 0, target - (e - 1), 0).astype(np.int64)
+
+
+def prescale_targets(scale: float) -> tuple[int, int]:
+    """(EA, EB) for s = 2^s_b: EA = min(14, 26 - s_b) keeps every hi finite
+    and every scaled residual below 2^16 (Rule 2, Sec. 4.2); EB = 14 - s_b also
+    keeps s * B_hi finite."""
+    s_b = int(np.frexp(np.float64(scale))[1]) - 1
+    return min(14, 26 - s_b), 14 - s_b
+
+
+def sgemm_prescaled(A, B, scale: float, order="elementwise", kb: int = DEFAULT_KB,
+                    threads: int | None = None) -> np.ndarray:
+    """SGEMM-cube on A' = diag(2^p) A and B' = B diag(2^q), then
+    C_ij = 2^-(p_i + q_j) C'_ij (each step exact unless it under/overflows)."""
+    A = np.ascontiguousarray(A, dtype=np.float32)
+    B = np.ascontiguousarray(B, dtype=np.float32)
+    ea, eb = prescale_targets(scale)
+    p = prescale_exponents(A, 1, ea)
+    q = prescale_exponents(B, 0, eb)
+    As = np.ldexp(A, p[:, None].astype(np.int32)).astype(np.float32)
+    Bs = np.ldexp(B, q[None, :].astype(np.int32)).astype(np.float32)
+    Cs = sgemm(As, Bs, scale, order, kb, threads)
+    return np.ldexp(Cs, (-(p[:, None] + q[None, :])).astype(np.int32)).astype(np.float32)
+
+
+RANGE_NONFINITE, RANGE_HI_OVERFLOW, RANGE_LO_OVERFLOW, RANGE_HI_SUBNORMAL = 1, 2, 4, 8
+
+
+def range_classes(X, scale: float) -> int:
+    """OR of the range classes of the entries of X under the split:
+    1 non-finite entry; 2 finite entry whose fl16 is infinite (|a| >= 65520);
+    4 finite hi whose scaled residual overflows FP16; 8 nonzero FP16-subnormal
+    hi."""
+    X = np.asarray(X, dtype=np.float32)
+    if X.size == 0:
+        return 0
+    hi, lo = split(X.reshape(1, -1), scale)
+    hi, lo = hi.ravel(), lo.ravel()
+    fin = np.isfinite(X.ravel())
+    hi_fin = (hi & 0x7C00) != 0x7C00
+    bits = 0
+    if (~fin).any():
+        bits |= RANGE_NONFINITE
+    if (fin & ~hi_fin).any():
+        bits |= RANGE_HI_OVERFLOW
+    if (hi_fin & ((lo & 0x7FFF) == 0x7C00)).any():
+        bits |= RANGE_LO_OVERFLOW
+    if (((hi & 0x7C00) == 0) & ((hi & 0x03FF) != 0)).any():
+        bits |= RANGE_HI_SUBNORMAL
+    return bits
+

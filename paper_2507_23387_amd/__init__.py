@@ -3,9 +3,10 @@
 Implements the SGEMM-cube method of arXiv 2507.23387: FP32 operands split into
 an FP16 high word and a scaled FP16 residual (Sec. 3.3), the product rebuilt
 from three FP16 GEMMs with FP32 accumulation (Eq. recover_eqn), in the
-elementwise or termwise order (Sec. 4.5).  All computation happens in the HIP
-kernels of ``libsgemmcube.so``; ``binding`` is the ctypes layer over its C-ABI
-(include/sgemm_cube.h).
+elementwise, termwise or cross-terms-first order (Sec. 4.5), with optional
+power-of-two pre-scaling and a range report (sgemm_cube_ex).  All computation
+happens in the HIP kernels of ``libsgemmcube.so``; ``binding`` is the ctypes
+layer over its C-ABI (include/sgemm_cube.h).
 """
 from .binding import (  # noqa: F401
     ELEMENTWISE,
@@ -13,9 +14,12 @@ from .binding import (  # noqa: F401
     SgemmCubeError,
     hgemm,
     matmul,
+    matmul_ex,
     sgemm_cube,
     sgemm_cube_block_k,
     sgemm_cube_compute,
+    sgemm_cube_ex,
+    sgemm_cube_ex_workspace_size,
     sgemm_cube_hgemm,
     sgemm_cube_prepare,
     sgemm_cube_split,

@@ -22,6 +22,12 @@ ELEMENTWISE_CROSS_FIRST = 2
 ORDERS = {"elementwise": ELEMENTWISE, "termwise": TERMWISE,
           "elementwise_cross_first": ELEMENTWISE_CROSS_FIRST}
 
+OPT_PRESCALE = 1
+RANGE_NONFINITE = 1
+RANGE_HI_OVERFLOW = 2
+RANGE_LO_OVERFLOW = 4
+RANGE_HI_SUBNORMAL = 8
+
 STATUS_OK = 0
 STATUS_NAMES = {
     0: "SGEMM_CUBE_OK",
@@ -33,9 +39,9 @@ STATUS_NAMES = {
 
 # Every symbol include/sgemm_cube.h declares.
 EXPORTS = (
-    "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_prepare", "sgemm_cube_compute",
-    "sgemm_cube_workspace_size", "sgemm_cube_split", "sgemm_cube_hgemm",
-    "sgemm_cube_status_string", "sgemm_cube_block_k",
+    "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_ex", "sgemm_cube_ex_workspace_size",
+    "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_workspace_size", "sgemm_cube_split",
+    "sgemm_cube_hgemm", "sgemm_cube_status_string", "sgemm_cube_block_k",
 )
 
 
@@ -51,12 +57,15 @@ def _load() -> ctypes.CDLL:
             f"{LIB_PATH} is not built; run `python -m paper_2507_23387_amd.build` "
             "(the HIP library is required, there is no fallback)")
     lib = ctypes.CDLL(LIB_PATH)
-    i64, ptr, f32, i32, sz = (ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_int,
-                              ctypes.c_size_t)
+    i64, ptr, f32, i32, sz, u32 = (ctypes.c_int64, ctypes.c_void_p, ctypes.c_float,
+                                   ctypes.c_int, ctypes.c_size_t, ctypes.c_uint)
     sig = {
         "sgemm_cube": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32, ptr]),
         "sgemm_cube_ws": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32, ptr, sz,
                                 ptr]),
+        "sgemm_cube_ex": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32, u32, ptr,
+                                sz, ptr, ptr]),
+        "sgemm_cube_ex_workspace_size": (sz, [i64, i64, i64, i32, u32]),
         "sgemm_cube_prepare": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, ptr, sz, ptr]),
         "sgemm_cube_compute": (i32, [i64, i64, i64, ptr, i64, f32, i32, ptr, sz, ptr]),
         "sgemm_cube_workspace_size": (sz, [i64, i64, i64, i32]),
@@ -85,6 +94,16 @@ def sgemm_cube_ws(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, ws, ws_by
                   stream) -> int:
     return _lib.sgemm_cube_ws(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, ws,
                               ws_bytes, stream)
+
+
+def sgemm_cube_ex(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, options, ws, ws_bytes,
+                  range_report, stream) -> int:
+    return _lib.sgemm_cube_ex(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, options, ws,
+                              ws_bytes, range_report, stream)
+
+
+def sgemm_cube_ex_workspace_size(M, N, K, accum_order=ELEMENTWISE, options=0) -> int:
+    return int(_lib.sgemm_cube_ex_workspace_size(M, N, K, accum_order, options))
 
 
 def sgemm_cube_prepare(M, N, K, A, lda, B, ldb, scale, ws, ws_bytes, stream) -> int:
@@ -162,6 +181,32 @@ def matmul(A, B, scale: float = 2.0**11, order="elementwise", out=None, workspac
                            _stream())
     _check(st, "sgemm_cube")
     return C
+
+
+def matmul_ex(A, B, scale: float = 2.0**11, order="elementwise", prescale: bool = False,
+              report: bool = False, out=None):
+    """sgemm_cube_ex on the current torch stream: optional power-of-two
+    pre-scaling of A's rows and B's columns; with report=True returns (C, bits)
+    where bits is a one-element int32 device tensor holding the range classes
+    (RANGE_*)."""
+    import torch
+
+    pa, lda = _mat(A, "A")
+    pb, ldb = _mat(B, "B")
+    M, K = A.shape
+    K2, N = B.shape
+    if K != K2:
+        raise ValueError(f"shape mismatch {tuple(A.shape)} x {tuple(B.shape)}")
+    C = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=A.device)
+    pc, ldc = _mat(C, "C")
+    options = OPT_PRESCALE if prescale else 0
+    n = sgemm_cube_ex_workspace_size(M, N, K, _order(order), options)
+    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=A.device)
+    bits = torch.zeros(1, dtype=torch.int32, device=A.device) if report else None
+    st = sgemm_cube_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, scale, _order(order), options,
+                       ws.data_ptr(), ws.numel(), bits.data_ptr() if report else None, _stream())
+    _check(st, "sgemm_cube_ex")
+    return (C, bits) if report else C
 
 
 def hgemm(A, B, out=None):

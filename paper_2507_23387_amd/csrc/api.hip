@@ -1,5 +1,6 @@
 // C-ABI of libsgemmcube: argument validation, workspace, dispatch.
 // The interface and its conventions are documented in include/sgemm_cube.h.
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdint>
@@ -11,7 +12,7 @@
 
 namespace sgc {
 
-Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base) {
+Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base, bool prescale) {
   Planes p{};
   p.Mp = round_up(M, kRowPad);
   p.Np = round_up(N, kRowPad);
@@ -26,6 +27,12 @@ Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base) {
   p.b_hi = reinterpret_cast<uint16_t*>(c + 2 * a_bytes);
   p.b_lo = reinterpret_cast<uint16_t*>(c + 2 * a_bytes + b_bytes);
   p.bytes = kFlagBytes + 2 * a_bytes + 2 * b_bytes;
+  if (prescale) {
+    // The row and column maxima follow the planes.
+    p.row_max = reinterpret_cast<uint32_t*>(c + 2 * a_bytes + 2 * b_bytes);
+    p.col_max = p.row_max + p.Mp;
+    p.bytes += static_cast<size_t>(round_up((p.Mp + p.Np) * 4, 256));
+  }
   return p;
 }
 
@@ -120,23 +127,51 @@ int current_cus() {
   return n;
 }
 
-size_t ws_size(int64_t M, int64_t N, int64_t K) {
+size_t ws_size(int64_t M, int64_t N, int64_t K, bool prescale = false) {
   if (M == 0 || N == 0 || K == 0) return 0;
-  return plan_planes(M, N, K, nullptr).bytes;
+  return plan_planes(M, N, K, nullptr, prescale).bytes;
 }
 
-// Enqueue the whole computation; arguments already validated.
+// Target exponents of the pre-scaled row (A) and column (B) maxima for
+// s = 2^s_b: [2^EA, 2^(EA+1)) with EA = min(14, 26 - s_b) keeps hi finite and
+// the scaled residual of every entry below 2^16 (Rule 2, Sec. 4.2); B's
+// EB = 14 - s_b also keeps s B_hi finite for the scaled elementwise kernel.
+RangeOpts range_opts(unsigned options, bool report, float scale) {
+  RangeOpts o;
+  o.prescale = (options & SGEMM_CUBE_OPT_PRESCALE) != 0;
+  o.report = report;
+  int e = 0;
+  (void)std::frexp(scale, &e);
+  const int s_b = e - 1;
+  o.exp_a = std::min(14, 26 - s_b);
+  o.exp_b = 14 - s_b;
+  return o;
+}
+
+// Enqueue the whole computation; arguments already validated.  `report`, if
+// not null, receives the range classes (device word).
 int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
         int64_t ldb, float* C, int64_t ldc, float scale, int variant, void* ws,
-        hipStream_t stream) {
-  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
-  if (K == 0) return launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
-                                                                     : SGEMM_CUBE_ERR_HIP;
-  const Planes p = plan_planes(M, N, K, ws);
-  if (launch_split_a(p, M, K, A, lda, scale, stream) != hipSuccess) return SGEMM_CUBE_ERR_HIP;
-  if (launch_split_b(p, K, N, B, ldb, scale, next_stamp(), stream) != hipSuccess)
+        hipStream_t stream, const RangeOpts& opt = RangeOpts{}, uint32_t* report = nullptr) {
+  if (M == 0 || N == 0 || K == 0) {
+    if (M > 0 && N > 0 && launch_zero(M, N, C, ldc, stream) != hipSuccess)
+      return SGEMM_CUBE_ERR_HIP;
+    if (report && launch_range_report(Planes{}, true, report, stream) != hipSuccess)
+      return SGEMM_CUBE_ERR_HIP;
+    return SGEMM_CUBE_OK;
+  }
+  const Planes p = plan_planes(M, N, K, ws, opt.prescale);
+  if (opt.prescale && launch_absmax(p, M, N, K, A, lda, B, ldb, stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (launch_split_a(p, M, K, A, lda, scale, opt, next_stamp(), stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (launch_split_b(p, K, N, B, ldb, scale, opt, next_stamp(), stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   if (launch_gemm(p, M, N, C, ldc, scale, variant, current_cus(), stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (opt.prescale && launch_unscale(p, M, N, C, ldc, opt, stream) != hipSuccess)
+    return SGEMM_CUBE_ERR_HIP;
+  if (report && launch_range_report(p, false, report, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   return SGEMM_CUBE_OK;
 }
@@ -223,6 +258,42 @@ int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
                   stream);
 }
 
+int sgemm_cube_ex(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
+                  int64_t ldb, float* C, int64_t ldc, float scale, int accum_order,
+                  unsigned options, void* ws, size_t ws_bytes, uint32_t* range_report,
+                  hipStream_t stream) {
+  if (!sgc::valid_order(accum_order) || (options & ~static_cast<unsigned>(SGEMM_CUBE_OPT_PRESCALE)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
+  if (st != SGEMM_CUBE_OK) return st;
+  const bool prescale = (options & SGEMM_CUBE_OPT_PRESCALE) != 0;
+  const size_t need = sgc::ws_size(M, N, K, prescale);
+  if (ws_bytes < need || (need > 0 && (!ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const uint64_t ab = sgc::span_bytes(M, K, lda, 4), bb = sgc::span_bytes(K, N, ldb, 4);
+  const uint64_t cb = sgc::span_bytes(M, N, ldc, 4);
+  if (need > 0 && (sgc::overlap(ws, need, A, ab) || sgc::overlap(ws, need, B, bb) ||
+                   sgc::overlap(ws, need, C, cb)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (range_report && (reinterpret_cast<uintptr_t>(range_report) % 4 != 0 ||
+                       sgc::overlap(range_report, 4, A, ab) ||
+                       sgc::overlap(range_report, 4, B, bb) ||
+                       sgc::overlap(range_report, 4, C, cb) ||
+                       sgc::overlap(range_report, 4, ws, need)))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  return sgc::run(M, N, K, A, lda, B, ldb, C, ldc, scale, sgc::variant_of(accum_order), ws,
+                  stream, sgc::range_opts(options, range_report != nullptr, scale), range_report);
+}
+
+size_t sgemm_cube_ex_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order,
+                                    unsigned options) {
+  if (!sgc::valid_order(accum_order) || (options & ~static_cast<unsigned>(SGEMM_CUBE_OPT_PRESCALE)))
+    return 0;
+  if (M < 0 || N < 0 || K < 0 || M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim)
+    return 0;
+  return sgc::ws_size(M, N, K, (options & SGEMM_CUBE_OPT_PRESCALE) != 0);
+}
+
 int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                        const float* B, int64_t ldb, float scale, void* ws, size_t ws_bytes,
                        hipStream_t stream) {
@@ -240,9 +311,12 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   const sgc::Planes p = sgc::plan_planes(M, N, K, ws);
-  if (A && sgc::launch_split_a(p, M, K, A, lda, scale, stream) != hipSuccess)
+  const sgc::RangeOpts plain;
+  if (A && sgc::launch_split_a(p, M, K, A, lda, scale, plain, sgc::next_stamp(), stream) !=
+               hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
-  if (B && sgc::launch_split_b(p, K, N, B, ldb, scale, sgc::next_stamp(), stream) != hipSuccess)
+  if (B && sgc::launch_split_b(p, K, N, B, ldb, scale, plain, sgc::next_stamp(), stream) !=
+               hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   return SGEMM_CUBE_OK;
 }

@@ -41,6 +41,17 @@ __host__ __device__ inline int64_t tiled_index(int64_t row, int64_t k, int64_t K
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// Pre-scaling shift of a row (column) whose largest finite magnitude has the
+// bits `max_bits`: the power of two that brings that magnitude into
+// [2^target, 2^(target+1)); 0 for an all-zero (or all non-finite) line.
+__device__ inline int prescale_shift(uint32_t max_bits, int target) {
+  const float m = __builtin_bit_cast(float, max_bits);
+  if (!(m > 0.0f) || !(m <= 3.4028235e38f)) return 0;
+  int e = 0;
+  (void)__builtin_frexpf(m, &e);
+  return target - (e - 1);
+}
+
 // Workspace: a header holding the range flag, then the four planes.  A planes
 // are Mp x Kp, B planes Np x Kp (B transposed), all tiled.  The range flag is
 // two words: range[0] == range[1] after the split of B exactly when some
@@ -49,6 +60,8 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 struct Planes {
   int64_t Mp, Np, Kp;
   uint32_t* range;
+  uint32_t* row_max;  // pre-scaling only: bits of each row's largest |A| (else null)
+  uint32_t* col_max;  // pre-scaling only: bits of each column's largest |B| (else null)
   uint16_t* a_hi;
   uint16_t* a_lo;
   uint16_t* b_hi;
@@ -56,7 +69,27 @@ struct Planes {
   size_t bytes;  // total workspace bytes
 };
 
-Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base);
+// Workspace header words (uint32).  Words 3..6 (A) and 7..10 (B) hold the
+// stamp of the split that saw an entry of range class 1, 2, 4, 8 (see
+// range_class in split.hip); compared with the split's own stamp word they
+// give the range report of the last split of each operand.
+constexpr int kWordBOverflow = 0;  // range flag: |B_hi| s > 65504 (stamped)
+constexpr int kWordBStamp = 1;
+constexpr int kWordAStamp = 2;
+constexpr int kWordAClass = 3;
+constexpr int kWordBClass = 7;
+constexpr int kRangeClasses = 4;
+
+// Options of one call: power-of-two pre-scaling of rows of A and columns of B
+// (target exponents of their largest magnitudes), and the range report.
+struct RangeOpts {
+  bool prescale = false;
+  bool report = false;
+  int exp_a = 0;
+  int exp_b = 0;
+};
+
+Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base, bool prescale = false);
 
 // Enqueue the split of a rows x cols row-major FP32 matrix into row-major
 // hi/lo planes with leading dimension ldh (the public split entry point).
@@ -65,16 +98,33 @@ hipError_t launch_split_rows(int64_t rows, int64_t cols, const float* X, int64_t
                              hipStream_t stream);
 
 // Enqueue the split of A (M x K row-major) into the tiled A planes,
-// zero-filling the padding up to Mp x Kp.
+// zero-filling the padding up to Mp x Kp; with opt.prescale row i is first
+// multiplied by its power of two (p.row_max), with opt.report the range
+// classes are stamped (`stamp`) into the workspace header.
 hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
-                          float scale, hipStream_t stream);
+                          float scale, const RangeOpts& opt, uint32_t stamp, hipStream_t stream);
 
 // Enqueue the split of B (K x N row-major) into the tiled, transposed B
 // planes (Np x Kp), zero-filling the padding, and recompute the range flag.
 // `stamp` must differ from the stamp of the previous split into the same
 // workspace (the C-ABI draws a fresh one per call).
 hipError_t launch_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
-                          float scale, uint32_t stamp, hipStream_t stream);
+                          float scale, const RangeOpts& opt, uint32_t stamp,
+                          hipStream_t stream);
+
+// Pre-scaling: enqueue the row maxima of |A| and column maxima of |B| (finite
+// entries only) into p.row_max / p.col_max.
+hipError_t launch_absmax(const Planes& p, int64_t M, int64_t N, int64_t K, const float* A,
+                         int64_t lda, const float* B, int64_t ldb, hipStream_t stream);
+
+// Pre-scaling: C_ij := 2^-(p_i + q_j) C_ij with the powers of two the splits
+// applied.
+hipError_t launch_unscale(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                          const RangeOpts& opt, hipStream_t stream);
+
+// Range report: *out := OR of the classes the last splits of A and B saw
+// (0 when `empty`, i.e. no split ran).
+hipError_t launch_range_report(const Planes& p, bool empty, uint32_t* out, hipStream_t stream);
 
 // Enqueue the MFMA GEMM on prepared planes.  `cus` is the device's compute
 // unit count (sizes the persistent grid of the 256 x 128 kernel).

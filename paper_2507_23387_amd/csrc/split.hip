@@ -86,18 +86,49 @@ __device__ __forceinline__ void split8(const float (&v)[8], float s, u32x4& hv, 
   }
 }
 
+// Range classes of one split entry a -> (hi, lo), after any pre-scaling:
+//   1  a is inf or NaN
+//   2  a is finite but fl16(a) is infinite (|a| >= 65520, Sec. 3.1)
+//   4  hi is finite but the scaled residual overflows FP16 (Rule 2, Sec. 4.2)
+//   8  hi is a nonzero FP16 subnormal (the 22-bit guarantee of Sec. 4.2 is lost)
+__device__ __forceinline__ uint32_t range_class(float a, uint16_t h, uint16_t l) {
+  const bool fin = __builtin_isfinite(a);
+  const bool h_fin = (h & 0x7c00) != 0x7c00;
+  uint32_t c = fin ? 0u : 1u;
+  if (fin && !h_fin) c |= 2u;
+  if (h_fin && (l & 0x7fff) == 0x7c00) c |= 4u;
+  if ((h & 0x7c00) == 0 && (h & 0x03ff) != 0) c |= 8u;
+  return c;
+}
+
+// Stamp the classes any lane of the wave saw into header words word..word+3
+// (one store per class and wave).
+__device__ __forceinline__ void report_classes(uint32_t cls, uint32_t* range, int word,
+                                               uint32_t stamp) {
+#pragma unroll
+  for (int b = 0; b < kRangeClasses; ++b) {
+    const unsigned long long m = __ballot((cls >> b) & 1u);
+    if (m && static_cast<int>(threadIdx.x & 63) == __ffsll(static_cast<long long>(m)) - 1)
+      range[word + b] = stamp;
+  }
+}
+
 // Split of A into the tiled planes.  A workgroup covers 16 rows x 128 k and a
 // wave 4 rows x 128 k: lane l takes 8 consecutive k of row l / 16, so each row
 // is read as one 512-byte piece, and the 16-byte chunks a store instruction
 // writes fill 8 whole 128-byte lines (4 rows x 32 bytes of one tile each).
 // blockIdx.y strides over row blocks.
-template <bool kVec>
+template <bool kVec, bool kPre, bool kReport>
 __global__ __launch_bounds__(256) void split_a_tiled_kernel(
     int64_t M, int64_t K, const float* __restrict__ X, int64_t ldx, uint16_t* __restrict__ hi,
-    uint16_t* __restrict__ lo, int64_t Mp, int64_t Kp, float s) {
+    uint16_t* __restrict__ lo, int64_t Mp, int64_t Kp, float s,
+    const uint32_t* __restrict__ row_max, int exp_a, uint32_t* __restrict__ range,
+    uint32_t stamp) {
   const int lane = threadIdx.x & 63;
   const int64_t k0 = static_cast<int64_t>(blockIdx.x) * 128 + (lane & 15) * 8;
+  if (kReport && threadIdx.x == 0) range[kWordAStamp] = stamp;
   if (k0 >= Kp) return;
+  uint32_t cls = 0;
   for (int64_t m = static_cast<int64_t>(blockIdx.y) * 16 + (threadIdx.x >> 6) * 4 + (lane >> 4);
        m < Mp; m += static_cast<int64_t>(gridDim.y) * 16) {
     float v[8];
@@ -110,12 +141,25 @@ __global__ __launch_bounds__(256) void split_a_tiled_kernel(
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? X[m * ldx + k0 + e] : 0.0f;
     }
+    if constexpr (kPre) {
+      const int shift = m < M ? prescale_shift(row_max[m], exp_a) : 0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = __builtin_ldexpf(v[e], shift);
+    }
     u32x4 hv, lv;
     split8(v, s, hv, lv);
+    if constexpr (kReport) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        cls |= range_class(v[2 * e], hv[e] & 0xffff, lv[e] & 0xffff);
+        cls |= range_class(v[2 * e + 1], hv[e] >> 16, lv[e] >> 16);
+      }
+    }
     const int64_t idx = tiled_index(m, k0, Kp);
     store_stream(hi + idx, hv);
     store_stream(lo + idx, lv);
   }
+  if constexpr (kReport) report_classes(cls, range, kWordAClass, stamp);
 }
 
 // Split of B (K x N row-major) into the tiled planes of B transposed.  One
@@ -126,10 +170,11 @@ __global__ __launch_bounds__(256) void split_a_tiled_kernel(
 // chunk t of both tiles of both planes (4 KiB contiguous per tile).  It also
 // stamps the range flag (see launch_split_b) when some |B_hi| s > 65504, the
 // largest finite FP16 value.
-template <bool kVec>
+template <bool kVec, bool kPre, bool kReport>
 __global__ __launch_bounds__(256) void split_b_tiled_kernel(
     int64_t K, int64_t N, const float* __restrict__ B, int64_t ldb, uint16_t* __restrict__ hi,
-    uint16_t* __restrict__ lo, int64_t Kp, float s, uint32_t* __restrict__ range, uint32_t stamp) {
+    uint16_t* __restrict__ lo, int64_t Kp, float s, const uint32_t* __restrict__ col_max,
+    int exp_b, uint32_t* __restrict__ range, uint32_t stamp) {
   constexpr int kK = 2 * kSlice;
   constexpr int kPitch = kK / 2 + 4;  // words per n row; 16-byte aligned rows
   __shared__ __align__(16) uint32_t ph[kPanel * kPitch];
@@ -157,7 +202,16 @@ __global__ __launch_bounds__(256) void split_b_tiled_kernel(
       v1[e] = (k + 1 < K && n + e < N) ? B[(k + 1) * ldb + n + e] : 0.0f;
     }
   }
+  if constexpr (kPre) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int shift = n + e < N ? prescale_shift(col_max[n + e], exp_b) : 0;
+      v0[e] = __builtin_ldexpf(v0[e], shift);
+      v1[e] = __builtin_ldexpf(v1[e], shift);
+    }
+  }
   bool big = false;
+  uint32_t cls = 0;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     uint16_t h0, l0, h1, l1;
@@ -165,11 +219,13 @@ __global__ __launch_bounds__(256) void split_b_tiled_kernel(
     split_value(v1[e], s, h1, l1);
     big |= __builtin_fabsf(static_cast<float>(__builtin_bit_cast(_Float16, h0))) * s > 65504.0f;
     big |= __builtin_fabsf(static_cast<float>(__builtin_bit_cast(_Float16, h1))) * s > 65504.0f;
+    if constexpr (kReport) cls |= range_class(v0[e], h0, l0) | range_class(v1[e], h1, l1);
     ph[(nl + e) * kPitch + kp] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
     pl[(nl + e) * kPitch + kp] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
   }
-  if (big) range[0] = stamp;
-  if (t == 0) range[1] = stamp;
+  if (big) range[kWordBOverflow] = stamp;
+  if (t == 0) range[kWordBStamp] = stamp;
+  if constexpr (kReport) report_classes(cls, range, kWordBClass, stamp);
   __syncthreads();
   const int r = t >> 1;
   const int c = (t & 1) ^ tile_swizzle(r);  // logical chunk stored at position t & 1
@@ -214,35 +270,63 @@ hipError_t launch_split_rows(int64_t rows, int64_t cols, const float* X, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
-                          float scale, hipStream_t stream) {
+namespace {
+
+template <bool kPre, bool kReport>
+void enqueue_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
+                     float scale, const RangeOpts& opt, uint32_t stamp, hipStream_t stream) {
   // Mp is a multiple of 256 and Kp of 64 (plan_planes).
   const dim3 grid(static_cast<unsigned>((p.Kp + 127) / 128), grid_rows(p.Mp / 16));
   const bool vec = (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (lda % 4 == 0);
   if (vec)
-    hipLaunchKernelGGL(split_a_tiled_kernel<true>, grid, dim3(256), 0, stream, M, K, A, lda,
-                       p.a_hi, p.a_lo, p.Mp, p.Kp, scale);
+    hipLaunchKernelGGL((split_a_tiled_kernel<true, kPre, kReport>), grid, dim3(256), 0, stream,
+                       M, K, A, lda, p.a_hi, p.a_lo, p.Mp, p.Kp, scale, p.row_max, opt.exp_a,
+                       p.range, stamp);
   else
-    hipLaunchKernelGGL(split_a_tiled_kernel<false>, grid, dim3(256), 0, stream, M, K, A, lda,
-                       p.a_hi, p.a_lo, p.Mp, p.Kp, scale);
+    hipLaunchKernelGGL((split_a_tiled_kernel<false, kPre, kReport>), grid, dim3(256), 0, stream,
+                       M, K, A, lda, p.a_hi, p.a_lo, p.Mp, p.Kp, scale, p.row_max, opt.exp_a,
+                       p.range, stamp);
+}
+
+template <bool kPre, bool kReport>
+void enqueue_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
+                     float scale, const RangeOpts& opt, uint32_t stamp, hipStream_t stream) {
+  // One workgroup per two tiles: Kp / 32 k blocks x Np / 128 panels (Np / 128
+  // <= 65535 is checked by the C-ABI).
+  const dim3 grid(static_cast<unsigned>(p.Kp / (2 * kSlice)), static_cast<unsigned>(p.Np / kPanel));
+  const bool vec = (reinterpret_cast<uintptr_t>(B) % 16 == 0) && (ldb % 4 == 0);
+  if (vec)
+    hipLaunchKernelGGL((split_b_tiled_kernel<true, kPre, kReport>), grid, dim3(256), 0, stream,
+                       K, N, B, ldb, p.b_hi, p.b_lo, p.Kp, scale, p.col_max, opt.exp_b, p.range,
+                       stamp);
+  else
+    hipLaunchKernelGGL((split_b_tiled_kernel<false, kPre, kReport>), grid, dim3(256), 0, stream,
+                       K, N, B, ldb, p.b_hi, p.b_lo, p.Kp, scale, p.col_max, opt.exp_b, p.range,
+                       stamp);
+}
+
+}  // namespace
+
+hipError_t launch_split_a(const Planes& p, int64_t M, int64_t K, const float* A, int64_t lda,
+                          float scale, const RangeOpts& opt, uint32_t stamp, hipStream_t stream) {
+  if (opt.prescale && opt.report) enqueue_split_a<true, true>(p, M, K, A, lda, scale, opt, stamp, stream);
+  else if (opt.prescale) enqueue_split_a<true, false>(p, M, K, A, lda, scale, opt, stamp, stream);
+  else if (opt.report) enqueue_split_a<false, true>(p, M, K, A, lda, scale, opt, stamp, stream);
+  else enqueue_split_a<false, false>(p, M, K, A, lda, scale, opt, stamp, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_split_b(const Planes& p, int64_t K, int64_t N, const float* B, int64_t ldb,
-                          float scale, uint32_t stamp, hipStream_t stream) {
-  // One workgroup per two tiles: Kp / 32 k blocks x Np / 128 panels (Np / 128
-  // <= 65535 is checked by the C-ABI).  Every workgroup writes range[1] =
-  // stamp and the ones that see an FP16 overflow of s B_hi write range[0] =
-  // stamp, so range[0] == range[1] afterwards exactly when this split found
-  // one; a fresh stamp per call makes a reset pass unnecessary.
-  const dim3 grid(static_cast<unsigned>(p.Kp / (2 * kSlice)), static_cast<unsigned>(p.Np / kPanel));
-  const bool vec = (reinterpret_cast<uintptr_t>(B) % 16 == 0) && (ldb % 4 == 0);
-  if (vec)
-    hipLaunchKernelGGL(split_b_tiled_kernel<true>, grid, dim3(256), 0, stream, K, N, B, ldb,
-                       p.b_hi, p.b_lo, p.Kp, scale, p.range, stamp);
-  else
-    hipLaunchKernelGGL(split_b_tiled_kernel<false>, grid, dim3(256), 0, stream, K, N, B, ldb,
-                       p.b_hi, p.b_lo, p.Kp, scale, p.range, stamp);
+                          float scale, const RangeOpts& opt, uint32_t stamp,
+                          hipStream_t stream) {
+  // Every workgroup writes range[kWordBStamp] = stamp and the ones that see
+  // an FP16 overflow of s B_hi write range[kWordBOverflow] = stamp, so the two
+  // words are equal afterwards exactly when this split found one; a fresh
+  // stamp per call makes a reset pass unnecessary.
+  if (opt.prescale && opt.report) enqueue_split_b<true, true>(p, K, N, B, ldb, scale, opt, stamp, stream);
+  else if (opt.prescale) enqueue_split_b<true, false>(p, K, N, B, ldb, scale, opt, stamp, stream);
+  else if (opt.report) enqueue_split_b<false, true>(p, K, N, B, ldb, scale, opt, stamp, stream);
+  else enqueue_split_b<false, false>(p, K, N, B, ldb, scale, opt, stamp, stream);
   return hipGetLastError();
 }
 

@@ -148,3 +148,31 @@ def test_hgemm_validation(lib):
                                 0) == INVALID
     assert lib.sgemm_cube_hgemm(0, 4, 4, FAKE, 4, FAKE + (1 << 30), 4, FAKE + (2 << 30), 4,
                                 0) == 0
+
+
+def call_ex(lib, M=4, N=4, K=4, options=0, ws=FAKE + (3 << 30), ws_bytes=1 << 20,
+            report=0, order=0):
+    return lib.sgemm_cube_ex(M, N, K, FAKE, K, FAKE + (1 << 30), N, FAKE + (2 << 30), N,
+                             2048.0, order, options, ws, ws_bytes, report, 0)
+
+
+def test_ex_validation(lib):
+    assert call_ex(lib, options=2) == INVALID                     # unknown option bit
+    assert call_ex(lib, order=3) == INVALID
+    assert call_ex(lib, ws_bytes=16) == INVALID                   # workspace too small
+    assert call_ex(lib, ws=FAKE + (3 << 30) + 8) == INVALID       # not 256-byte aligned
+    assert call_ex(lib, report=FAKE + (3 << 30) + 2) == INVALID   # report not 4-byte aligned
+    assert call_ex(lib, report=FAKE + 4) == INVALID               # report overlaps A
+    assert call_ex(lib, report=FAKE + (3 << 30) + 64) == INVALID  # report inside the workspace
+    # Only validation runs: M = 0 returns before device work when no report is asked for.
+    assert call_ex(lib, M=0, options=1) == 0
+
+
+def test_ex_workspace_size(lib):
+    base = lib.sgemm_cube_workspace_size(300, 200, 100)
+    assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 0) == base
+    # Pre-scaling adds the row and column maxima (Mp + Np words, 256-byte rounded).
+    assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 1) == base + (512 + 256) * 4
+    assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 2) == 0
+    assert lib.sgemm_cube_ex_workspace_size(300, 200, 0, 2, 1) == 0
+
