@@ -132,6 +132,9 @@ def main():
     ap.add_argument("--workload", default="c3")
     ap.add_argument("--order", default=None, help="elementwise | termwise | elementwise_cross_first")
     ap.add_argument("--scale", type=float, default=None)
+    ap.add_argument("--stages", type=int, default=0,
+                    help="elementwise only: LDS stage slots of the 256x256 kernel (1-4; "
+                         "0 = the library's default), through sgemm_cube_compute_stages")
     ap.add_argument("--prescale", action="store_true",
                     help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -176,8 +179,13 @@ def main():
             raise sgc.SgemmCubeError(st, "sgemm_cube_prepare")
 
     def compute():
-        st = sgc.sgemm_cube_compute(M, N, K, dC.data_ptr(), N, scale, order_code, ws.data_ptr(),
-                                    ws_bytes, sh)
+        if args.stages:
+            st = sgc.binding.sgemm_cube_compute_stages(M, N, K, dC.data_ptr(), N, scale,
+                                                       order_code, args.stages, ws.data_ptr(),
+                                                       ws_bytes, sh)
+        else:
+            st = sgc.sgemm_cube_compute(M, N, K, dC.data_ptr(), N, scale, order_code,
+                                        ws.data_ptr(), ws_bytes, sh)
         if st:
             raise sgc.SgemmCubeError(st, "sgemm_cube_compute")
 
@@ -287,7 +295,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "seed": w.seed,
                    "distribution": w.dist, "scale": scale, "order": order,
-                   **({"prescale": True} if args.prescale else {})},
+                   **({"prescale": True} if args.prescale else {}),
+                   **({"stages": args.stages} if args.stages else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,
         **extra,

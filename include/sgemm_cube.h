@@ -171,6 +171,23 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
                        int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Measurement hook for the pipeline ablation (Sec. 5.4 measures double
+ * buffering against a single buffer): sgemm_cube_compute with the elementwise
+ * order, running the 256 x 256 kernel with `stages` LDS stage slots,
+ * 1 <= stages <= 4.  stages = 1 copies each k-step's operands into LDS and
+ * waits for them inside the step (no prefetch); stages = S >= 2 keeps the
+ * copies of S - 1 later steps in flight; the library's own choice is 4.
+ * Results are identical for every stage count.  accum_order other than
+ * SGEMM_CUBE_ELEMENTWISE -> SGEMM_CUBE_ERR_NOT_SUPPORTED; stages outside
+ * 1..4 -> SGEMM_CUBE_ERR_INVALID_VALUE; otherwise as sgemm_cube_compute
+ * (when the range flag selects the unscaled fallback kernel, that kernel
+ * keeps its own pipeline).
+ */
+int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
+                              float scale, int accum_order, int stages, const void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
 /* Device workspace in bytes that sgemm_cube_ws needs for this problem
  * (0 for degenerate shapes); 0 also for invalid arguments. */
 size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order);

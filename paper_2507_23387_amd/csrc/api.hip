@@ -223,6 +223,33 @@ int run_allocating(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
   return st;
 }
 
+// sgemm_cube_compute and sgemm_cube_compute_stages; stages == 0 means the
+// library's default pipeline.
+int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale, int accum_order,
+            int stages, const void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !valid_scale(scale))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (stages < 0 || stages > 4) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (stages != 0 && accum_order != SGEMM_CUBE_ELEMENTWISE) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
+  if (!C || !ld_ok(M, ldc)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (K == 0)
+    return launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK : SGEMM_CUBE_ERR_HIP;
+  const size_t need = ws_size(M, N, K);
+  if (ws_bytes < need || !ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (overlap(ws, need, C, span_bytes(M, N, ldc, 4))) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const Planes p = plan_planes(M, N, K, const_cast<void*>(ws));
+  const hipError_t e =
+      stages == 0
+          ? launch_gemm(p, M, N, C, ldc, scale, variant_of(accum_order), current_cus(), stream)
+          : launch_gemm_stages(p, M, N, C, ldc, scale, stages, current_cus(), stream);
+  return e == hipSuccess ? SGEMM_CUBE_OK : SGEMM_CUBE_ERR_HIP;
+}
+
 }  // namespace
 }  // namespace sgc
 
@@ -323,27 +350,14 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 
 int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
                        int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !sgc::valid_scale(scale))
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
-  if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
-  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
-  if (!C || !sgc::ld_ok(M, ldc)) return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (K == 0)
-    return sgc::launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
-                                                                : SGEMM_CUBE_ERR_HIP;
-  const size_t need = sgc::ws_size(M, N, K);
-  if (ws_bytes < need || !ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (sgc::overlap(ws, need, C, sgc::span_bytes(M, N, ldc, 4)))
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
-  const sgc::Planes p = sgc::plan_planes(M, N, K, const_cast<void*>(ws));
-  return sgc::launch_gemm(p, M, N, C, ldc, scale, sgc::variant_of(accum_order),
-                         sgc::current_cus(), stream) ==
-                 hipSuccess
-             ? SGEMM_CUBE_OK
-             : SGEMM_CUBE_ERR_HIP;
+  return sgc::compute(M, N, K, C, ldc, scale, accum_order, 0, ws, ws_bytes, stream);
+}
+
+int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,
+                              float scale, int accum_order, int stages, const void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+  if (stages < 1) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  return sgc::compute(M, N, K, C, ldc, scale, accum_order, stages, ws, ws_bytes, stream);
 }
 
 size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order) {

@@ -163,20 +163,23 @@ constexpr int kWideStages = 4;
 template <int V>
 constexpr int wide_planes() { return V == kElementwise ? 4 : 2; }
 
-template <int V>
+template <int V, int S>
 constexpr size_t wide_lds_bytes() {
-  return static_cast<size_t>(kWideStages) * wide_planes<V>() * kWide * kSlice * 2;
+  return static_cast<size_t>(S) * wide_planes<V>() * kWide * kSlice * 2;
 }
 
-template <int V>
+// S = number of LDS stage slots.  S >= 2: the DMAs of stage kt+S are in flight
+// while steps kt+1 .. kt+S-1 compute.  S = 1 (no prefetch, for the pipeline
+// ablation): the next stage is copied and waited for inside each step.
+template <int V, int S>
 __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
   static_assert(V == kElementwise || V == kHiOnly, "wide kernel variants");
+  static_assert(S >= 1 && S <= 4 && (V == kElementwise || S >= 2), "stage count");
   constexpr bool kEl = V == kElementwise;
-  constexpr int S = kWideStages;
   constexpr int kPlanes = wide_planes<V>();       // LDS slots: A_hi, B_hi, A_lo, B_lo
   constexpr int kPlaneHalves = kWide * kSlice;    // two tiles
   constexpr int kStageHalves = kPlanes * kPlaneHalves;
@@ -267,10 +270,19 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
         for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bs[j], acc[i][j]);
         SCHED_FENCE();
         if (i == 0) {
-          wait_vmcnt<(S - 2) * kDma>();
-          lds_barrier();
+          if constexpr (S == 1) {
+            // Retire the single slot, copy stage kt+1 into it and wait.
+            lds_barrier();
+#pragma unroll
+            for (int n = 0; n < kDma; ++n) dma_one(nk, n);
+            wait_vmcnt<0>();
+            lds_barrier();
+          } else {
+            wait_vmcnt<(S - 2) * kDma>();
+            lds_barrier();
+          }
         }
-        dma_next();
+        if constexpr (S > 1) dma_next();
         SCHED_FENCE();
       }
 #pragma unroll
@@ -279,7 +291,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
         for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(al[i], bh[j], acc[i][j]);
         SCHED_FENCE();
         al[i] = rd(nk, kAL, aoff[i]);
-        dma_next();
+        if constexpr (S > 1) dma_next();
         SCHED_FENCE();
       }
 #pragma unroll
@@ -536,15 +548,15 @@ hipError_t set_lds(Kern kernel, size_t bytes) {
                              static_cast<int>(bytes));
 }
 
-template <int V>
+template <int V, int S = kWideStages>
 hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
                        hipStream_t stream) {
-  constexpr size_t lds = wide_lds_bytes<V>();
-  static const hipError_t attr = set_lds(&gemm_wide_kernel<V>, lds);
+  constexpr size_t lds = wide_lds_bytes<V, S>();
+  static const hipError_t attr = set_lds(&gemm_wide_kernel<V, S>, lds);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kWide);
   const int tiles_n = static_cast<int>(p.Np / kWide);
-  hipLaunchKernelGGL(gemm_wide_kernel<V>, dim3(tiles_m * tiles_n), dim3(kWideThreads), lds,
+  hipLaunchKernelGGL((gemm_wide_kernel<V, S>), dim3(tiles_m * tiles_n), dim3(kWideThreads), lds,
                      stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
                      static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
                      static_cast<int>(N), s, 1.0f / s);
@@ -584,6 +596,20 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
     case kHiOnly: return launch_wide<kHiOnly>(p, M, N, C, ldc, scale, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                              float scale, int stages, int cus, hipStream_t stream) {
+  hipError_t e = hipSuccess;
+  switch (stages) {
+    case 1: e = launch_wide<kElementwise, 1>(p, M, N, C, ldc, scale, stream); break;
+    case 2: e = launch_wide<kElementwise, 2>(p, M, N, C, ldc, scale, stream); break;
+    case 3: e = launch_wide<kElementwise, 3>(p, M, N, C, ldc, scale, stream); break;
+    case 4: e = launch_wide<kElementwise, 4>(p, M, N, C, ldc, scale, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (e != hipSuccess) return e;
+  return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
 }
 
 }  // namespace sgc

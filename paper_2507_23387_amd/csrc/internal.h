@@ -131,6 +131,12 @@ hipError_t launch_range_report(const Planes& p, bool empty, uint32_t* out, hipSt
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                        float scale, int variant, int cus, hipStream_t stream);
 
+// The elementwise GEMM with an explicit number of LDS stage slots of the
+// 256 x 256 kernel (1..4; the library's default is 4), for the pipeline
+// ablation.  The fallback kernel (range flag set) keeps its own depth.
+hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                              float scale, int stages, int cus, hipStream_t stream);
+
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);

@@ -176,3 +176,14 @@ def test_ex_workspace_size(lib):
     assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 2) == 0
     assert lib.sgemm_cube_ex_workspace_size(300, 200, 0, 2, 1) == 0
 
+
+def test_compute_stages_validation(lib):
+    ws = FAKE + (3 << 30)
+    call = lambda order=0, stages=2, M=4: lib.sgemm_cube_compute_stages(
+        M, 4, 4, FAKE, 4, 2048.0, order, stages, ws, 1 << 20, 0)
+    assert call(stages=0) == INVALID
+    assert call(stages=5) == INVALID
+    assert call(order=1) == NOT_SUPPORTED
+    assert call(order=2) == NOT_SUPPORTED
+    assert call(M=0, stages=1) == 0          # validation only: M = 0 is a no-op
+
