@@ -72,12 +72,12 @@ __device__ __forceinline__ floatx16 mfma32(const half8& a, const half8& b, const
 }
 
 // One 64-lane LDS DMA: lane l copies 16 bytes from g into LDS byte address
-// lds_addr + 16 * l.  Inline asm, so the compiler adds no conservative vmcnt(0)
-// before later LDS reads; the kernels wait explicitly with wait_vmcnt<>()
-// before the barrier that publishes a stage.
+// lds_addr + 16 * l (the instruction takes the LDS base from M0, which the
+// "{m0}" operand has the compiler load).  Inline asm, so the compiler adds no
+// conservative vmcnt(0) before later LDS reads; the kernels wait explicitly
+// with wait_vmcnt<>() before the barrier that publishes a stage.
 __device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_addr)
-               : "memory", "m0");
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_addr) : "memory");
 }
 
 template <int N>
