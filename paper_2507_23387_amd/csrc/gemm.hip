@@ -51,6 +51,7 @@
 // the slot of stage kt before it is refilled.  Past the last stage the loads
 // repeat the last stage, so every wait count is a compile-time constant.
 #include <algorithm>
+#include <atomic>
 
 #include "internal.h"
 
@@ -541,18 +542,29 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
   }
 }
 
+// Raise a kernel's dynamic-LDS limit on the current device, once per device
+// and kernel (each instantiation calls this with its own `done` table).
+constexpr int kMaxDevices = 64;
 template <typename Kern>
-hipError_t set_lds(Kern kernel, size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                             static_cast<int>(bytes));
+hipError_t set_lds(Kern kernel, size_t bytes, std::atomic<bool> (&done)[kMaxDevices]) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < kMaxDevices && done[dev].load(std::memory_order_acquire))
+    return hipSuccess;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
+  if (e == hipSuccess && dev >= 0 && dev < kMaxDevices)
+    done[dev].store(true, std::memory_order_release);
+  return e;
 }
 
 template <int V, int S = kWideStages>
 hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
                        hipStream_t stream) {
   constexpr size_t lds = wide_lds_bytes<V, S>();
-  static const hipError_t attr = set_lds(&gemm_wide_kernel<V, S>, lds);
+  static std::atomic<bool> done[kMaxDevices];
+  const hipError_t attr = set_lds(&gemm_wide_kernel<V, S>, lds, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kWide);
   const int tiles_n = static_cast<int>(p.Np / kWide);
@@ -566,7 +578,8 @@ hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
 template <int V>
 hipError_t launch_narrow(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
                          int cus, hipStream_t stream) {
-  static const hipError_t attr = set_lds(&gemm_narrow_kernel<V>, kNarrowLdsBytes);
+  static std::atomic<bool> done[kMaxDevices];
+  const hipError_t attr = set_lds(&gemm_narrow_kernel<V>, kNarrowLdsBytes, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kNarrowM);
   const int tiles_n = static_cast<int>(p.Np / kNarrowN);
