@@ -55,7 +55,7 @@ class SgemmCubeError(RuntimeError):
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is not built; run `python -m paper_2507_23387_amd.build` "
+            f"{LIB_PATH} is not built; run `python -m paper_2507_23387_amd.build` or `__graft_entry__.build()` "
             "(the HIP library is required, there is no fallback)")
     lib = ctypes.CDLL(LIB_PATH)
     i64, ptr, f32, i32, sz, u32 = (ctypes.c_int64, ctypes.c_void_p, ctypes.c_float,
