@@ -54,7 +54,7 @@ typedef enum {
   SGEMM_CUBE_ELEMENTWISE_CROSS_FIRST = 2  /* the reordering proposed at the end of
                                              Sec. 4.5: per block g,
                                              acc = acc + ((XA_g + XB_g) / s + HH_g),
-                                             blocks of 2 * sgemm_cube_block_k() */
+                                             blocks of sgemm_cube_block_k() */
 } sgemm_cube_order_t;
 
 /* Status codes returned by every entry point. */
@@ -174,13 +174,14 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
 /*
  * Measurement hook for the pipeline ablation (Sec. 5.4 measures double
  * buffering against a single buffer): sgemm_cube_compute with the elementwise
- * order, running the 256 x 256 kernel with `stages` LDS stage slots,
- * 1 <= stages <= 4.  stages = 1 copies each k-step's operands into LDS and
- * waits for them inside the step (no prefetch); stages = S >= 2 keeps the
- * copies of S - 1 later steps in flight; the library's own choice is 4.
- * Results are identical for every stage count.  accum_order other than
- * SGEMM_CUBE_ELEMENTWISE -> SGEMM_CUBE_ERR_NOT_SUPPORTED; stages outside
- * 1..4 -> SGEMM_CUBE_ERR_INVALID_VALUE; otherwise as sgemm_cube_compute
+ * order, running the 256 x 256 kernel with `stages` LDS stage slots of one
+ * 32-wide k-step each (64 KiB), 1 <= stages <= 2.  stages = 1 copies each
+ * k-step's operands into LDS and waits for them inside the step (no
+ * prefetch); stages = 2 (the library's own choice) keeps the copy of the next
+ * step in flight while a step computes.  Results are identical for both stage
+ * counts.  accum_order other than SGEMM_CUBE_ELEMENTWISE ->
+ * SGEMM_CUBE_ERR_NOT_SUPPORTED; stages outside 1..2 ->
+ * SGEMM_CUBE_ERR_INVALID_VALUE; otherwise as sgemm_cube_compute
  * (when the range flag selects the unscaled fallback kernel, that kernel
  * keeps its own pipeline).
  */
@@ -217,14 +218,15 @@ int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t ld
 /* Static, human-readable name of a status code. */
 const char* sgemm_cube_status_string(int status);
 
-/* Size in elements of the elementwise k-block g of Eq. elementwise on the
- * main path (16, one MFMA k-step): there the running accumulator holds
+/* Size in elements of the elementwise k-block g of Eq. elementwise (32). On
+ * the main path a block is one MFMA k-step: the running accumulator holds
  * scale * acc and each block's three products are summed into it by the
  * matrix unit in the order HH, XA, XB, each sum rounded once together with
  * the accumulator.  When some |fl16(B)| * scale exceeds 65504 (scale * B_hi
  * would overflow FP16) the elementwise order runs unscaled with blocks of
- * twice this size instead: HH into the accumulator, XA_g and XB_g summed
- * separately, acc = (acc + XA_g / s) + XB_g / s. */
+ * the same size instead: HH into the accumulator, XA_g and XB_g summed
+ * separately, acc = (acc + XA_g / s) + XB_g / s.  The cross-terms-first order
+ * uses the same block size. */
 int sgemm_cube_block_k(void);
 
 #ifdef __cplusplus

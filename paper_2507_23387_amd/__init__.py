@@ -41,8 +41,10 @@ __all__ = list(_EXPORTS)
 
 
 def __getattr__(name):
-    if name in _EXPORTS:
-        from . import binding  # raises ImportError if libsgemmcube.so is missing
+    if name in _EXPORTS or name == "binding":
+        import importlib
 
-        return getattr(binding, name)
+        # Raises ImportError if libsgemmcube.so is missing.
+        binding = importlib.import_module(__name__ + ".binding")
+        return binding if name == "binding" else getattr(binding, name)
     raise AttributeError(f"module {__name__!r} has no attribute {name!r}")

@@ -230,7 +230,7 @@ int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
   if (!valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !valid_scale(scale))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (stages < 0 || stages > 4) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (stages < 0 || stages > 2) return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (stages != 0 && accum_order != SGEMM_CUBE_ELEMENTWISE) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   if (round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;

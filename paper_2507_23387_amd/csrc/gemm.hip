@@ -60,6 +60,7 @@ namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kKSteps = kSlice / 16;  // MFMA k-steps per tile slice (1)
 static_assert(kKSteps == 1, "one MFMA k-step per slice");
@@ -156,22 +157,54 @@ __device__ __forceinline__ void store_tile(float* __restrict__ C, int64_t ldc, i
 }
 
 // ---------------------------------------------------------------------------
-// 256 x 256 tiles: scaled elementwise and hi-only.
+// 256 x 256 tiles: scaled elementwise and hi-only, on v_mfma_f32_16x16x32_f16.
+//
+// The 16 x 16 x 32 form is used here because under the board's power limit it
+// sustains a higher FP16 rate on random operands than the 32 x 32 x 16 form
+// (less energy per product, so a higher shader clock at the same power).
 constexpr int kWide = 256;
 constexpr int kWideThreads = 256;
-constexpr int kWideStages = 4;
+constexpr int kWideStages = 2;
+constexpr int kStep = 2 * kSlice;  // k per MFMA step of the wide kernel (32): two slices
+
+// D(16x16) = A(16x32) B(32x16) + C.  Lane l supplies A row l%16 and B column
+// l%16 with the 8 consecutive k values 8*(l/16) .. 8*(l/16)+7 of the 32-wide
+// step; D element (row 4*(l/16) + r, column l%16) is in register r.
+__device__ __forceinline__ floatx4 mfma16(const half8& a, const half8& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
 
 template <int V>
 constexpr int wide_planes() { return V == kElementwise ? 4 : 2; }
 
 template <int V, int S>
 constexpr size_t wide_lds_bytes() {
-  return static_cast<size_t>(S) * wide_planes<V>() * kWide * kSlice * 2;
+  return static_cast<size_t>(S) * wide_planes<V>() * kWide * kStep * 2;
 }
 
-// S = number of LDS stage slots.  S >= 2: the DMAs of stage kt+S are in flight
-// while steps kt+1 .. kt+S-1 compute.  S = 1 (no prefetch, for the pipeline
-// ablation): the next stage is copied and waited for inside each step.
+// Store a wave's 16 x 16 accumulators: register r of MFMA tile (i, j) holds
+// row 4*(l/16) + r and column l%16 of that tile.  `value` maps (i, j, r) to
+// the float to store.  Tiles entirely inside C take the unmasked path.
+template <int kSubM, int kSubN, typename F>
+__device__ __forceinline__ void store_tile16(float* __restrict__ C, int64_t ldc, int M, int N,
+                                             int row0, int col0, bool full, F value) {
+  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
+#pragma unroll
+  for (int i = 0; i < kSubM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rr = i * 16 + r;
+      float* const p = base + static_cast<int64_t>(rr) * ldc;
+#pragma unroll
+      for (int j = 0; j < kSubN; ++j)
+        if (full || (row0 + rr < M && col0 + j * 16 < N)) p[j * 16] = value(i, j, r);
+    }
+}
+
+// S = number of LDS stage slots, one 32-k step each (64 KiB with four planes).
+// S = 2: the DMAs of stage kt+2 are in flight while step kt+1 computes.
+// S = 1 (no prefetch, for the pipeline ablation): the next stage is copied and
+// waited for inside each step.
 template <int V, int S>
 __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
@@ -179,13 +212,13 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
   static_assert(V == kElementwise || V == kHiOnly, "wide kernel variants");
-  static_assert(S >= 1 && S <= 4 && (V == kElementwise || S >= 2), "stage count");
+  static_assert((S == 1 && V == kElementwise) || S == 2, "stage count");
   constexpr bool kEl = V == kElementwise;
   constexpr int kPlanes = wide_planes<V>();       // LDS slots: A_hi, B_hi, A_lo, B_lo
-  constexpr int kPlaneHalves = kWide * kSlice;    // two tiles
+  constexpr int kPlaneHalves = kWide * kStep;     // two panels x two slices: four tiles
   constexpr int kStageHalves = kPlanes * kPlaneHalves;
-  constexpr int kDma = kPlanes * 2;               // 1 KiB DMAs per wave per stage
-  constexpr int kSub = 4;                         // 32 x 32 MFMA tiles per wave side
+  constexpr int kDma = kPlanes * 4;               // 1 KiB DMAs per wave per stage
+  constexpr int kSub = 8;                         // 16 x 16 MFMA tiles per wave side
   if constexpr (kEl) {
     if (range[0] == range[1]) return;  // s B_hi overflows FP16: the narrow kernel runs instead
   }
@@ -197,10 +230,11 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
   const int64_t slices = Kp / kSlice;
-  const int ktiles = static_cast<int>(slices);
+  const int ksteps = static_cast<int>(slices / 2);
 
-  // Wave w copies 1 KiB block w of both tiles (panel 2t and 2t+1) of each
-  // plane per stage: 32 rows of 16 k.
+  // A stage holds, per plane, the tiles (panel ph, slice sl) of the tile's two
+  // panels and the step's two slices at tile position 2*ph + sl.  Wave w copies
+  // 1 KiB block w of each of those four tiles.
   const int64_t panel_stride = slices * kTileHalves;
   const uint16_t* src[4] = {a_hi + 2 * tm * panel_stride, b_hi + 2 * tn * panel_stride,
                             kEl ? a_lo + 2 * tm * panel_stride : nullptr,
@@ -208,33 +242,35 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   const int64_t lane_off = w * 512 + lane * 8;
   const unsigned lds_base = lds_address(lds);
   auto dma_one = [&](int kt, int n) {  // n-th DMA of stage kt, n < kDma
-    const int ktc = min(kt, ktiles - 1);
-    const int p = n >> 1, half = n & 1;
+    const int ktc = min(kt, ksteps - 1);
+    const int p = n >> 2, ph = (n >> 1) & 1, sl = n & 1;
     const unsigned dst = lds_base + ((kt % S) * kStageHalves + p * kPlaneHalves +
-                                     (half * 4 + w) * 512) * 2;
-    dma16(src[p] + half * panel_stride + static_cast<int64_t>(ktc) * kTileHalves + lane_off, dst);
+                                     (2 * ph + sl) * kTileHalves + w * 512) * 2;
+    dma16(src[p] + ph * panel_stride + static_cast<int64_t>(2 * ktc + sl) * kTileHalves +
+              lane_off, dst);
   };
 
-  const int fr = lane & 31, fk = lane >> 5;
-  int aoff[kSub], boff[kSub];
-#pragma unroll
-  for (int i = 0; i < kSub; ++i) {
-    aoff[i] = frag_offset(wm * 128 + i * 32 + fr, fk);
-    boff[i] = frag_offset(wn * 128 + i * 32 + fr, fk);
-  }
-  auto rd = [&](int kt, int slot, int off) -> half8 {
-    return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + slot * kPlaneHalves +
-                                           off);
-  };
+  // Fragment of block i (rows 16 i .. 16 i + 15 of this wave's 128 rows, which
+  // are panel wm of A / panel wn of B): lane l reads row 16 i + l%16, k chunk
+  // c = l/16 of the step, i.e. chunk c%2 of slice c/2.
+  const int fr = lane & 15, fc = lane >> 4;
+  const int row_off = fr * kSlice + (((fc & 1) ^ tile_swizzle(fr)) << 3);
+  const int a_off = (2 * wm + (fc >> 1)) * kTileHalves + row_off;
+  const int b_off = (2 * wn + (fc >> 1)) * kTileHalves + row_off;
   constexpr int kAH = 0, kBH = 1, kAL = 2, kBL = 3;
+  auto rd = [&](int kt, int plane, int i) -> half8 {
+    const int off = (plane == kAH || plane == kAL) ? a_off : b_off;
+    return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + plane * kPlaneHalves +
+                                           off + i * 16 * kSlice);
+  };
   const _Float16 s16 = static_cast<_Float16>(s);
 
-  floatx16 acc[kSub][kSub];
+  floatx4 acc[kSub][kSub];
 #pragma unroll
   for (int i = 0; i < kSub; ++i)
 #pragma unroll
-    for (int j = 0; j < kSub; ++j) acc[i][j] = floatx16{};
-  half8 ah[kSub], al[kSub], bh[kSub], bs[kSub], bl[kSub];
+    for (int j = 0; j < kSub; ++j) acc[i][j] = floatx4{};
+  half8 ah[kSub], bh[kSub];
 
 #pragma unroll
   for (int st = 0; st < S; ++st)
@@ -242,23 +278,24 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
     for (int n = 0; n < kDma; ++n) dma_one(st, n);
   wait_vmcnt<(S - 1) * kDma>();
   lds_barrier();
-#pragma unroll
-  for (int i = 0; i < kSub; ++i) {
-    ah[i] = rd(0, kAH, aoff[i]);
-    bh[i] = rd(0, kBH, boff[i]);
-    if constexpr (kEl) {
-      al[i] = rd(0, kAL, aoff[i]);
-      bl[i] = rd(0, kBL, boff[i]);
-      bs[i] = bh[i] * s16;
-    }
-  }
 
   if constexpr (kEl) {
+    half8 al[kSub], bs[kSub], bl[kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+      ah[i] = rd(0, kAH, i);
+      bh[i] = rd(0, kBH, i);
+      al[i] = rd(0, kAL, i);
+      bl[i] = rd(0, kBL, i);
+      bs[i] = bh[i] * s16;
+    }
     // One k-step: G1 = HH (A_hi x sB_hi), G2 = XA (A_lo x B_hi), G3 = XB
     // (A_hi x B_lo), each row by row, in this order for every accumulator.
-    // The fragments of step kt+1 come from stage kt+1; A_hi row i is
-    // reloaded after its last use in G3 and first needed again 12 MFMAs later,
-    // in row i of the next G1.
+    // The fragments of step kt+1 come from stage kt+1; each register is
+    // reloaded after its last use in step kt: A_lo row i after its G2 row,
+    // A_hi row i after its G3 row (first needed again in row i of the next G1),
+    // B_hi during G3 rows 0-3 and s B_hi formed from it in rows 4-7, B_lo
+    // after G3.
     auto step = [&](int kt) {
       const int nk = kt + 1;
       int dn = 0;
@@ -268,7 +305,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
 #pragma unroll
       for (int i = 0; i < kSub; ++i) {
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bs[j], acc[i][j]);
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(ah[i], bs[j], acc[i][j]);
         SCHED_FENCE();
         if (i == 0) {
           if constexpr (S == 1) {
@@ -289,59 +326,64 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
 #pragma unroll
       for (int i = 0; i < kSub; ++i) {
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(al[i], bh[j], acc[i][j]);
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(al[i], bh[j], acc[i][j]);
         SCHED_FENCE();
-        al[i] = rd(nk, kAL, aoff[i]);
+        al[i] = rd(nk, kAL, i);
         if constexpr (S > 1) dma_next();
         SCHED_FENCE();
       }
 #pragma unroll
       for (int i = 0; i < kSub; ++i) {
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ah[i], bl[j], acc[i][j]);
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(ah[i], bl[j], acc[i][j]);
         SCHED_FENCE();
-        ah[i] = rd(nk, kAH, aoff[i]);
-        if (i < 2) {
-          bh[2 * i] = rd(nk, kBH, boff[2 * i]);
-          bh[2 * i + 1] = rd(nk, kBH, boff[2 * i + 1]);
+        ah[i] = rd(nk, kAH, i);
+        if (i < kSub / 2) {
+          bh[2 * i] = rd(nk, kBH, 2 * i);
+          bh[2 * i + 1] = rd(nk, kBH, 2 * i + 1);
         } else {
-          bs[2 * (i - 2)] = bh[2 * (i - 2)] * s16;
-          bs[2 * (i - 2) + 1] = bh[2 * (i - 2) + 1] * s16;
+          bs[2 * i - kSub] = bh[2 * i - kSub] * s16;
+          bs[2 * i - kSub + 1] = bh[2 * i - kSub + 1] * s16;
         }
         SCHED_FENCE();
       }
 #pragma unroll
-      for (int j = 0; j < kSub; ++j) bl[j] = rd(nk, kBL, boff[j]);
+      for (int j = 0; j < kSub; ++j) bl[j] = rd(nk, kBL, j);
     };
-    for (int kt = 0; kt < ktiles; kt += 2) {
+    for (int kt = 0; kt < ksteps; kt += 2) {
       step(kt);
       step(kt + 1);
     }
   } else {
-    // Hi-only: double-buffered fragments (they are few), read right after the
-    // barrier of each step.
+    // Hi-only: double-buffered fragments, read right after the barrier of
+    // each step.
     half8 ah2[kSub], bh2[kSub];
+#pragma unroll
+    for (int i = 0; i < kSub; ++i) {
+      ah[i] = rd(0, kAH, i);
+      bh[i] = rd(0, kBH, i);
+    }
     auto step = [&](int kt, half8 (&ac)[kSub], half8 (&bc)[kSub], half8 (&an)[kSub],
                     half8 (&bn)[kSub]) {
 #pragma unroll
       for (int i = 0; i < kSub; ++i) {
 #pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma32(ac[i], bc[j], acc[i][j]);
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(ac[i], bc[j], acc[i][j]);
         SCHED_FENCE();
         if (i == 0) {
           wait_vmcnt<(S - 2) * kDma>();
           lds_barrier();
 #pragma unroll
           for (int q = 0; q < kSub; ++q) {
-            an[q] = rd(kt + 1, kAH, aoff[q]);
-            bn[q] = rd(kt + 1, kBH, boff[q]);
+            an[q] = rd(kt + 1, kAH, q);
+            bn[q] = rd(kt + 1, kBH, q);
           }
         }
         dma_one(kt + S, i);
         SCHED_FENCE();
       }
     };
-    for (int kt = 0; kt < ktiles; kt += 2) {
+    for (int kt = 0; kt < ksteps; kt += 2) {
       step(kt, ah, bh, ah2, bh2);
       step(kt + 1, ah2, bh2, ah, bh);
     }
@@ -350,13 +392,12 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   wait_vmcnt<0>();
 
   const float out_scale = kEl ? inv_s : 1.0f;
-  const int col0 = tn * kWide + wn * 128 + (lane & 31);
-  const int row0 = tm * kWide + wm * 128 + (lane >> 5) * 4;
+  const int col0 = tn * kWide + wn * 128 + (lane & 15);
+  const int row0 = tm * kWide + wm * 128 + (lane >> 4) * 4;
   const bool full = (tm + 1) * kWide <= M && (tn + 1) * kWide <= N;
-  store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full,
-                         [&](int i, int j, int r) { return acc[i][j][r] * out_scale; });
+  store_tile16<kSub, kSub>(C, ldc, M, N, row0, col0, full,
+                           [&](int i, int j, int r) { return acc[i][j][r] * out_scale; });
 }
-
 // ---------------------------------------------------------------------------
 // 256 x 128 tiles: termwise and the unscaled elementwise fallback.
 constexpr int kNarrowM = 256;
@@ -617,8 +658,6 @@ hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, i
   switch (stages) {
     case 1: e = launch_wide<kElementwise, 1>(p, M, N, C, ldc, scale, stream); break;
     case 2: e = launch_wide<kElementwise, 2>(p, M, N, C, ldc, scale, stream); break;
-    case 3: e = launch_wide<kElementwise, 3>(p, M, N, C, ldc, scale, stream); break;
-    case 4: e = launch_wide<kElementwise, 4>(p, M, N, C, ldc, scale, stream); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

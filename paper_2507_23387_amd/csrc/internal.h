@@ -23,7 +23,7 @@ enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2, kCrossFirst =
 // so that the MFMA fragment reads from LDS (32 rows, one chunk each) spread
 // over all banks.  The GEMM copies tiles into LDS verbatim.
 constexpr int kPanel = 128;                     // rows per panel
-constexpr int kSlice = 16;                      // k per tile = one MFMA k-step
+constexpr int kSlice = 16;                      // k per tile
 constexpr int kTileHalves = kPanel * kSlice;    // 2048 halves = 4 KiB
 constexpr int kRowPad = 256;                    // M and N are padded to this
 constexpr int kKPad = 64;                       // K is padded to this
@@ -132,7 +132,7 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
                        float scale, int variant, int cus, hipStream_t stream);
 
 // The elementwise GEMM with an explicit number of LDS stage slots of the
-// 256 x 256 kernel (1..4; the library's default is 4), for the pipeline
+// 256 x 256 kernel (1 or 2; the library's default is 2), for the pipeline
 // ablation.  The fallback kernel (range flag set) keeps its own depth.
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, int cus, hipStream_t stream);
@@ -141,10 +141,10 @@ hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, i
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);
 
-// The elementwise k-block of the scaled kernel (one MFMA k-step), and of the
-// fallback kernel used when the range flag is set and of the cross-terms-first
-// order (two k-steps).
-constexpr int kBlockScaled = kSlice;
+// The elementwise k-block of the scaled kernel (one 16 x 16 x 32 MFMA k-step),
+// and of the fallback kernel used when the range flag is set and of the
+// cross-terms-first order (two 32 x 32 x 16 MFMA k-steps).
+constexpr int kBlockScaled = 2 * kSlice;
 constexpr int kBlockFallback = 2 * kSlice;
 
 }  // namespace sgc

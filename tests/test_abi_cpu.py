@@ -46,7 +46,7 @@ def test_status_strings(lib):
 
 
 def test_block_k(lib):
-    assert lib.sgemm_cube_block_k() == 16
+    assert lib.sgemm_cube_block_k() == 32
 
 
 def test_workspace_size(lib):
@@ -182,7 +182,7 @@ def test_compute_stages_validation(lib):
     call = lambda order=0, stages=2, M=4: lib.sgemm_cube_compute_stages(
         M, 4, 4, FAKE, 4, 2048.0, order, stages, ws, 1 << 20, 0)
     assert call(stages=0) == INVALID
-    assert call(stages=5) == INVALID
+    assert call(stages=3) == INVALID
     assert call(order=1) == NOT_SUPPORTED
     assert call(order=2) == NOT_SUPPORTED
     assert call(M=0, stages=1) == 0          # validation only: M = 0 is a no-op

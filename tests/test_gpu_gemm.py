@@ -2,7 +2,7 @@
 
 Bar: |C_gpu - C_oracle|_ij <= 2 K 2^-24 (|A||B|)_ij for every compared entry,
 equality where (|A||B|)_ij = 0, identical inf/NaN patterns.  The oracle runs
-with the GPU's elementwise block size (sgemm_cube_block_k() = 16), so both
+with the GPU's elementwise block size (sgemm_cube_block_k() = 32), so both
 sides fold the same blocks g of Eq. elementwise; the summation inside a block
 differs (MFMA versus sequential, and on the scaled path each block term is
 rounded together with the accumulator), which the bar covers.
@@ -29,12 +29,12 @@ SHAPES = [
 
 
 def _kb(order="elementwise"):
-    """The oracle's block size matching the GPU's: one MFMA k-step, two for the
-    cross-terms-first order."""
+    """The oracle's block size matching the GPU's (the same for every order:
+    one 16 x 16 x 32 MFMA k-step on the scaled elementwise kernel, two
+    32 x 32 x 16 k-steps on the 256 x 128 kernel)."""
     from paper_2507_23387_amd import binding
 
-    kb = binding.sgemm_cube_block_k()
-    return 2 * kb if order == "elementwise_cross_first" else kb
+    return binding.sgemm_cube_block_k()
 
 
 @pytest.mark.parametrize("order", ORDERS)

@@ -1,6 +1,7 @@
 """How the matrix unit sums FP16 x FP16 products into FP32, probed through the
 C-ABI (sgemm_cube_hgemm on FP16-exact inputs, so hi = a and the kernel is a
-chain of v_mfma_f32_32x32x16_f16 starting from zero).
+chain of v_mfma_f32_16x16x32_f16 starting from zero, one k-step of
+sgemm_cube_block_k() = 32 products per instruction).
 
 The parity tolerance rests on these properties (the paper assumes an RN FP32
 accumulation in the matrix unit, Sec. 4.3, and names checking it as open work,
@@ -69,11 +70,14 @@ def test_accumulator_plus_products_of_the_next_k_step(gpu):
     """1 in the accumulator (first k-step), 2^-24 + 2^-30 as products of the
     second k-step: one rounding of the exact sum, 1 + 2^-23 (sequential
     round-to-nearest would give 1)."""
-    a = np.zeros(32)
-    b = np.zeros(32)
+    from paper_2507_23387_amd import binding
+
+    kb = binding.sgemm_cube_block_k()
+    a = np.zeros(2 * kb)
+    b = np.zeros(2 * kb)
     a[0] = b[0] = 1.0
-    a[16], b[16] = 2.0**-12, 2.0**-12
-    a[17], b[17] = 2.0**-15, 2.0**-15
+    a[kb], b[kb] = 2.0**-12, 2.0**-12
+    a[kb + 1], b[kb + 1] = 2.0**-15, 2.0**-15
     log("mfma numerics accumulator")
     got = _dot(a, b)
     assert got == 1.0 + 2.0**-23

@@ -12,6 +12,12 @@ from tests.helpers import abs_ab, assert_parity
 pytestmark = pytest.mark.gpu
 
 
+def _kb():
+    from paper_2507_23387_amd import binding
+
+    return binding.sgemm_cube_block_k()
+
+
 def _run(A, B, stages_list, scale=2048.0):
     import torch
 
@@ -45,10 +51,10 @@ def test_every_stage_count_computes_the_same_bits(gpu, shape):
     M, N, K = shape
     A, B = workloads.make_operands(M, N, K, M + 2 * N + K, "normal")
     log(f"pipeline stages {shape}")
-    res = _run(A, B, [0, 1, 2, 3, 4])
-    for st in (1, 2, 3, 4):
+    res = _run(A, B, [0, 1, 2])
+    for st in (1, 2):
         assert np.array_equal(res[st].view(np.uint32), res[0].view(np.uint32)), st
-    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=16)
+    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
     assert_parity(res[1], Co, K, abs_ab(A, B), f"stages {shape}")
 
 
@@ -56,9 +62,8 @@ def test_stage_counts_on_the_4096_cube_sampled_rows(gpu):
     w = workloads.get("c2")
     A, B = workloads.workload_operands(w)
     log("pipeline stages c2")
-    res = _run(A, B, [0, 1, 3])
+    res = _run(A, B, [0, 1])
     assert np.array_equal(res[1].view(np.uint32), res[0].view(np.uint32))
-    assert np.array_equal(res[3].view(np.uint32), res[0].view(np.uint32))
     rows = workloads.sample_rows(w.M, 8, w.seed)
-    Co = oracle.sgemm_rows(A, B, rows, 2048.0, "elementwise", kb=16)
+    Co = oracle.sgemm_rows(A, B, rows, 2048.0, "elementwise", kb=_kb())
     assert_parity(res[1][rows], Co, w.K, abs_ab(A, B, rows), "stages c2")

@@ -96,7 +96,7 @@ def test_prescaled_subnormal_hi_workload(gpu):
     coef = float(bounds.main_bound_coef(w.K))
     assert np.all(np.abs(pre.astype(np.float64) - ref64(A, B, rows)) <= coef * abs_ab(A, B, rows))
     As, Bs = _prescaled_inputs(A, B, 2048.0)
-    Cs = oracle.sgemm_rows(As, Bs, rows, 2048.0, "termwise", kb=16)
+    Cs = oracle.sgemm_rows(As, Bs, rows, 2048.0, "termwise", kb=32)
     _assert_unscaled_parity(pre, Cs, A, B, rows, w.K)
 
 
