@@ -54,7 +54,8 @@ def kernel_source_hash() -> str:
     """Hash of the sources the GEMM kernel is built from (ties a committed
     HBM-traffic measurement to the kernel it was taken on)."""
     h = hashlib.sha256()
-    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/internal.h"):
+    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/gemm_fused.hip",
+                "paper_2507_23387_amd/csrc/gemm_common.h", "paper_2507_23387_amd/csrc/internal.h"):
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -135,6 +136,9 @@ def main():
     ap.add_argument("--stages", type=int, default=0,
                     help="elementwise only: LDS stage slots of the 256x256 kernel (1-4; "
                          "0 = the library's default), through sgemm_cube_compute_stages")
+    ap.add_argument("--fused", action="store_true",
+                    help="elementwise only: time sgemm_cube_compute_a, whose GEMM kernel splits A "
+                         "in registers (the split pass then covers B only)")
     ap.add_argument("--prescale", action="store_true",
                     help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -172,14 +176,23 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
+    # --fused (elementwise only): a step is the split of B (sgemm_cube_prepare
+    # with A = NULL) and sgemm_cube_compute_a, whose kernel splits A in
+    # registers; by default a step is the split of both operands and the GEMM
+    # on the tiled planes, which is what sgemm_cube_ws enqueues.
+    fused = args.fused and order == "elementwise" and not args.stages
+
     def prepare():
-        st = sgc.sgemm_cube_prepare(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, scale,
-                                    ws.data_ptr(), ws_bytes, sh)
+        st = sgc.sgemm_cube_prepare(M, N, K, None if fused else dA.data_ptr(), K, dB.data_ptr(),
+                                    N, scale, ws.data_ptr(), ws_bytes, sh)
         if st:
             raise sgc.SgemmCubeError(st, "sgemm_cube_prepare")
 
     def compute():
-        if args.stages:
+        if fused:
+            st = sgc.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), K, dC.data_ptr(), N, scale,
+                                          order_code, ws.data_ptr(), ws_bytes, sh)
+        elif args.stages:
             st = sgc.binding.sgemm_cube_compute_stages(M, N, K, dC.data_ptr(), N, scale,
                                                        order_code, args.stages, ws.data_ptr(),
                                                        ws_bytes, sh)
@@ -246,7 +259,7 @@ def main():
     traffic = traffic_entry(w.name, order)
     roofline = {
         "bound": "mfma",
-        "kernel": GEMM_KERNELS[order],
+        "kernel": "gemm_fused_a_kernel" if fused else GEMM_KERNELS[order],
         "achieved": gemm_tflops,
         "peak": FP16_PEAK_TFLOPS,
         "unit": "TFLOP/s",
@@ -255,7 +268,9 @@ def main():
         "algorithmic_flops_per_launch": 3 * flops,
         "avg_launch_ms": gemm_ms,
     }
-    split_bytes = 8.0 * (M * K + K * N)  # 4 B read + 2 x 2 B written per element
+    # 4 B read + 2 x 2 B written per element split (B only when A is split in
+    # the GEMM kernel).
+    split_bytes = 8.0 * ((0 if fused else M * K) + K * N)
     extra = {
         "pct_of_3gemm_peak": 100 * value / THREE_GEMM_PEAK_TFLOPS,
         "three_gemm_peak_tflops": THREE_GEMM_PEAK_TFLOPS,
@@ -296,6 +311,7 @@ def main():
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "seed": w.seed,
                    "distribution": w.dist, "scale": scale, "order": order,
                    **({"prescale": True} if args.prescale else {}),
+                   **({"fused_split_a": True} if fused else {}),
                    **({"stages": args.stages} if args.stages else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,

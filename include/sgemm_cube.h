@@ -172,6 +172,31 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
                        int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The second half of sgemm_cube_ws for a workspace whose B planes are
+ * prepared (sgemm_cube_prepare with A == NULL): splits A (Sec. 3.3) and runs
+ * the three-product GEMM (Eq. recover_eqn, Sec. 4.5), reading A as FP32.
+ * Gives the same bits as sgemm_cube_ws(...), i.e. as prepare(A = NULL, B)
+ * followed by prepare(A, B = NULL) and compute.
+ * For the elementwise order, when A is 16-byte aligned and lda and K are
+ * multiples of 4, the split of A happens inside the GEMM kernel (in
+ * registers, with the same arithmetic as the split kernels, so the result is
+ * the same) and the A planes are not written unless the scaled kernel cannot
+ * run (some |fl16(B)| * scale > 65504); no pass over A goes through HBM
+ * besides the GEMM's own reads.  Otherwise A is split into the workspace
+ * first.  (On MI355X the fused kernel is slower than the split pass plus the
+ * GEMM on the tiled planes, which sgemm_cube and sgemm_cube_ws use: its reads
+ * of row-major FP32 A, 128 bytes from each of 256 rows per k-step, cost more
+ * than the split pass saves.)
+ * M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes and the errors
+ * follow sgemm_cube_ws; C must not overlap A or the workspace.  Must use the
+ * same M, N, K and scale as the prepare of B (the library cannot check this).
+ * Afterwards the workspace's A planes are unspecified.
+ */
+int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                         float* C, int64_t ldc, float scale, int accum_order, void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/*
  * Measurement hook for the pipeline ablation (Sec. 5.4 measures double
  * buffering against a single buffer): sgemm_cube_compute with the elementwise
  * order, running the 256 x 256 kernel with `stages` LDS stage slots of one

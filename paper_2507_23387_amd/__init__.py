@@ -24,6 +24,7 @@ _EXPORTS = (
     "sgemm_cube",
     "sgemm_cube_block_k",
     "sgemm_cube_compute",
+    "sgemm_cube_compute_a",
     "sgemm_cube_compute_stages",
     "sgemm_cube_ex",
     "sgemm_cube_ex_workspace_size",

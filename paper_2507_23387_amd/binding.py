@@ -40,7 +40,8 @@ STATUS_NAMES = {
 # Every symbol include/sgemm_cube.h declares.
 EXPORTS = (
     "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_ex", "sgemm_cube_ex_workspace_size",
-    "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_stages",
+    "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_a",
+    "sgemm_cube_compute_stages",
     "sgemm_cube_workspace_size", "sgemm_cube_split",
     "sgemm_cube_hgemm", "sgemm_cube_status_string", "sgemm_cube_block_k",
 )
@@ -69,6 +70,8 @@ def _load() -> ctypes.CDLL:
         "sgemm_cube_ex_workspace_size": (sz, [i64, i64, i64, i32, u32]),
         "sgemm_cube_prepare": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, ptr, sz, ptr]),
         "sgemm_cube_compute": (i32, [i64, i64, i64, ptr, i64, f32, i32, ptr, sz, ptr]),
+        "sgemm_cube_compute_a": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, i32, ptr, sz,
+                                       ptr]),
         "sgemm_cube_compute_stages": (i32, [i64, i64, i64, ptr, i64, f32, i32, i32, ptr, sz,
                                             ptr]),
         "sgemm_cube_workspace_size": (sz, [i64, i64, i64, i32]),
@@ -115,6 +118,12 @@ def sgemm_cube_prepare(M, N, K, A, lda, B, ldb, scale, ws, ws_bytes, stream) -> 
 
 def sgemm_cube_compute(M, N, K, C, ldc, scale, accum_order, ws, ws_bytes, stream) -> int:
     return _lib.sgemm_cube_compute(M, N, K, C, ldc, scale, accum_order, ws, ws_bytes, stream)
+
+
+def sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes,
+                         stream) -> int:
+    return _lib.sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes,
+                                     stream)
 
 
 def sgemm_cube_compute_stages(M, N, K, C, ldc, scale, accum_order, stages, ws, ws_bytes,

@@ -148,6 +148,29 @@ RangeOpts range_opts(unsigned options, bool report, float scale) {
   return o;
 }
 
+// sgemm_cube_compute_a: the elementwise order splits A inside the GEMM
+// (gemm_fused.hip) when A's rows can be read as 16-byte vectors.
+bool fused_a_ok(const float* A, int64_t lda, int64_t K, int variant) {
+  return variant == kElementwise && reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 &&
+         K % 4 == 0;
+}
+
+// GEMM from FP32 A and a workspace whose B planes are prepared: the fused
+// elementwise kernel when it applies, else the split of A and the GEMM on the
+// planes.
+hipError_t compute_from_a(const Planes& p, int64_t M, int64_t N, int64_t K, const float* A,
+                          int64_t lda, float* C, int64_t ldc, float scale, int variant,
+                          hipStream_t stream) {
+  if (fused_a_ok(A, lda, K, variant)) {
+    const hipError_t e = launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, stream);
+    if (e != hipSuccess) return e;
+    return launch_gemm_fallback(p, M, N, C, ldc, scale, current_cus(), stream);
+  }
+  const hipError_t e = launch_split_a(p, M, K, A, lda, scale, RangeOpts{}, next_stamp(), stream);
+  if (e != hipSuccess) return e;
+  return launch_gemm(p, M, N, C, ldc, scale, variant, current_cus(), stream);
+}
+
 // Enqueue the whole computation; arguments already validated.  `report`, if
 // not null, receives the range classes (device word).
 int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
@@ -351,6 +374,35 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
                        int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream) {
   return sgc::compute(M, N, K, C, ldc, scale, accum_order, 0, ws, ws_bytes, stream);
+}
+
+int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                         float* C, int64_t ldc, float scale, int accum_order, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M < 0 || N < 0 || K < 0 || lda < (K > 1 ? K : 1) || ldc < (N > 1 ? N : 1) ||
+      !sgc::valid_scale(scale))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if ((M > 0 && K > 0 && !A) || (M > 0 && N > 0 && !C)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::ld_ok(M, lda) || !sgc::ld_ok(M, ldc)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  const uint64_t ab = sgc::span_bytes(M, K, lda, 4), cb = sgc::span_bytes(M, N, ldc, 4);
+  if (sgc::overlap(C, cb, A, ab)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
+  if (K == 0)
+    return sgc::launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
+                                                                : SGEMM_CUBE_ERR_HIP;
+  const size_t need = sgc::ws_size(M, N, K);
+  if (ws_bytes < need || !ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (sgc::overlap(ws, need, A, ab) || sgc::overlap(ws, need, C, cb))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const sgc::Planes p = sgc::plan_planes(M, N, K, ws);
+  return sgc::compute_from_a(p, M, N, K, A, lda, C, ldc, scale, sgc::variant_of(accum_order),
+                             stream) == hipSuccess
+             ? SGEMM_CUBE_OK
+             : SGEMM_CUBE_ERR_HIP;
 }
 
 int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,

@@ -53,108 +53,14 @@
 #include <algorithm>
 #include <atomic>
 
-#include "internal.h"
+#include "gemm_common.h"
 
 namespace sgc {
 namespace {
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-
 constexpr int kKSteps = kSlice / 16;  // MFMA k-steps per tile slice (1)
 static_assert(kKSteps == 1, "one MFMA k-step per slice");
 static_assert(kKPad % (2 * kSlice) == 0, "the main loops take two slices per iteration");
-
-// D(32x32) = A(32x16) B(16x32) + C.  Lane l supplies A row l%32 and B column
-// l%32 with the 8 consecutive k values 8*(l/32) .. 8*(l/32)+7 of the 16-wide
-// step; D element (row 8*(r/4) + 4*(l/32) + r%4, column l%32) is in register r.
-__device__ __forceinline__ floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
-}
-
-// One 64-lane LDS DMA: lane l copies 16 bytes from g into LDS byte address
-// lds_addr + 16 * l (the instruction takes the LDS base from M0, which the
-// "{m0}" operand has the compiler load).  Inline asm, so the compiler adds no
-// conservative vmcnt(0) before later LDS reads; the kernels wait explicitly
-// with wait_vmcnt<>() before the barrier that publishes a stage.
-__device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_addr) : "memory");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// This wave's LDS reads are complete, then all waves meet.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// Keeps the instruction groups of the schedule in program order.
-#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
-
-// Offset (halves) of the fragment of LDS row r for k chunk fk (0 or 1).
-__device__ __forceinline__ int frag_offset(int r, int fk) {
-  return r * kSlice + ((fk ^ tile_swizzle(r)) << 3);
-}
-
-// LDS byte address of the dynamic shared-memory base (the M0 operand of the
-// DMA): cast the generic pointer to the LDS address space, then to int.
-__device__ __forceinline__ unsigned lds_address(const uint16_t* p) {
-  return static_cast<unsigned>((uintptr_t)((__attribute__((address_space(3))) const uint16_t*)p));
-}
-
-// Map a tile index to a (tile_m, tile_n) pair.  Workgroups are dispatched
-// round-robin over the 8 XCDs, so index i runs on XCD i % 8 (also for the
-// persistent grid, whose size is a multiple of 8); renumbering gives each XCD
-// a contiguous range of logical tiles, and grouping kGroup tile-rows keeps the
-// A and B panels a group touches resident in that XCD's L2.
-template <int kGroup>
-__device__ __forceinline__ void tile_of(int index, int tiles_m, int tiles_n, int& tm, int& tn) {
-  const int nwg = tiles_m * tiles_n;
-  int wg = index;
-  if ((nwg & 7) == 0) wg = (wg & 7) * (nwg >> 3) + (wg >> 3);
-  const int per_group = kGroup * tiles_n;
-  const int group = wg / per_group;
-  const int first_m = group * kGroup;
-  const int gsize = min(tiles_m - first_m, kGroup);
-  const int in_group = wg - group * per_group;
-  tm = first_m + in_group % gsize;
-  tn = in_group / gsize;
-}
-
-// Store a wave's accumulators: register r of MFMA tile (i, j) holds row
-// 8*(r/4) + 4*(l/32) + r%4 and column l%32 of that 32 x 32 tile.  `value`
-// maps (i, j, r) to the float to store.  Tiles entirely inside C take the
-// unmasked path; row offsets are wave-uniform multiples of ldc.
-template <int kSubM, int kSubN, typename F>
-__device__ __forceinline__ void store_tile(float* __restrict__ C, int64_t ldc, int M, int N,
-                                           int row0, int col0, bool full, F value) {
-  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
-  if (full) {
-#pragma unroll
-    for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float* const p = base + static_cast<int64_t>(i * 32 + (r >> 2) * 8 + (r & 3)) * ldc;
-#pragma unroll
-        for (int j = 0; j < kSubN; ++j) p[j * 32] = value(i, j, r);
-      }
-  } else {
-#pragma unroll
-    for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int rr = i * 32 + (r >> 2) * 8 + (r & 3);
-        float* const p = base + static_cast<int64_t>(rr) * ldc;
-#pragma unroll
-        for (int j = 0; j < kSubN; ++j)
-          if (row0 + rr < M && col0 + j * 32 < N) p[j * 32] = value(i, j, r);
-      }
-  }
-}
 
 // ---------------------------------------------------------------------------
 // 256 x 256 tiles: scaled elementwise and hi-only, on v_mfma_f32_16x16x32_f16.
@@ -167,12 +73,6 @@ constexpr int kWideThreads = 256;
 constexpr int kWideStages = 2;
 constexpr int kStep = 2 * kSlice;  // k per MFMA step of the wide kernel (32): two slices
 
-// D(16x16) = A(16x32) B(32x16) + C.  Lane l supplies A row l%16 and B column
-// l%16 with the 8 consecutive k values 8*(l/16) .. 8*(l/16)+7 of the 32-wide
-// step; D element (row 4*(l/16) + r, column l%16) is in register r.
-__device__ __forceinline__ floatx4 mfma16(const half8& a, const half8& b, const floatx4& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
 
 template <int V>
 constexpr int wide_planes() { return V == kElementwise ? 4 : 2; }
@@ -182,24 +82,6 @@ constexpr size_t wide_lds_bytes() {
   return static_cast<size_t>(S) * wide_planes<V>() * kWide * kStep * 2;
 }
 
-// Store a wave's 16 x 16 accumulators: register r of MFMA tile (i, j) holds
-// row 4*(l/16) + r and column l%16 of that tile.  `value` maps (i, j, r) to
-// the float to store.  Tiles entirely inside C take the unmasked path.
-template <int kSubM, int kSubN, typename F>
-__device__ __forceinline__ void store_tile16(float* __restrict__ C, int64_t ldc, int M, int N,
-                                             int row0, int col0, bool full, F value) {
-  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
-#pragma unroll
-  for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int rr = i * 16 + r;
-      float* const p = base + static_cast<int64_t>(rr) * ldc;
-#pragma unroll
-      for (int j = 0; j < kSubN; ++j)
-        if (full || (row0 + rr < M && col0 + j * 16 < N)) p[j * 16] = value(i, j, r);
-    }
-}
 
 // S = number of LDS stage slots, one 32-k step each (64 KiB with four planes).
 // S = 2: the DMAs of stage kt+2 are in flight while step kt+1 computes.
@@ -225,7 +107,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
-  tile_of<4>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn))
+    tile_of<4>(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
@@ -252,14 +135,19 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
 
   // Fragment of block i (rows 16 i .. 16 i + 15 of this wave's 128 rows, which
   // are panel wm of A / panel wn of B): lane l reads row 16 i + l%16, k chunk
-  // c = l/16 of the step, i.e. chunk c%2 of slice c/2.
+  // c = l/16 of the step, i.e. chunk c%2 of slice c/2.  The chunk swap of the
+  // tile layout depends on bit 4 of the row, i.e. on the parity of i.
   const int fr = lane & 15, fc = lane >> 4;
-  const int row_off = fr * kSlice + (((fc & 1) ^ tile_swizzle(fr)) << 3);
-  const int a_off = (2 * wm + (fc >> 1)) * kTileHalves + row_off;
-  const int b_off = (2 * wn + (fc >> 1)) * kTileHalves + row_off;
+  int a_off[2], b_off[2];
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const int row_off = fr * kSlice + (((fc & 1) ^ tile_swizzle(16 * par + fr)) << 3);
+    a_off[par] = (2 * wm + (fc >> 1)) * kTileHalves + row_off;
+    b_off[par] = (2 * wn + (fc >> 1)) * kTileHalves + row_off;
+  }
   constexpr int kAH = 0, kBH = 1, kAL = 2, kBL = 3;
   auto rd = [&](int kt, int plane, int i) -> half8 {
-    const int off = (plane == kAH || plane == kAL) ? a_off : b_off;
+    const int off = (plane == kAH || plane == kAL) ? a_off[i & 1] : b_off[i & 1];
     return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + plane * kPlaneHalves +
                                            off + i * 16 * kSlice);
   };
@@ -270,44 +158,51 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   for (int i = 0; i < kSub; ++i)
 #pragma unroll
     for (int j = 0; j < kSub; ++j) acc[i][j] = floatx4{};
-  half8 ah[kSub], bh[kSub];
 
+  // Prologue: stage 0 (each step copies the next stage).
 #pragma unroll
-  for (int st = 0; st < S; ++st)
-#pragma unroll
-    for (int n = 0; n < kDma; ++n) dma_one(st, n);
-  wait_vmcnt<(S - 1) * kDma>();
+  for (int n = 0; n < kDma; ++n) dma_one(0, n);
+  wait_vmcnt<0>();
   lds_barrier();
 
   if constexpr (kEl) {
-    half8 al[kSub], bs[kSub], bl[kSub];
+    // Row-fused schedule: for each row i of 16 x 16 blocks the wave issues
+    // HH(i, .), then XA(i, .), then XB(i, .), so every accumulator still sees
+    // the block terms in the order HH, XA, XB.  The B fragments of the whole
+    // step stay in registers (s B_hi, B_hi, B_lo); A fragments are needed one
+    // row at a time and are read one row ahead.  The two B_hi register sets
+    // swap roles every step: after HH of row 7 the set that held s B_hi
+    // receives the next step's B_hi, and after XA of row 7 the other set
+    // receives s times it.  One barrier per step, before row 7, publishes
+    // stage kt+1 (row 7 reads the next step's fragments from it) and retires
+    // the slot of stage kt; the DMAs of stage kt+1 are issued in rows 0-5 of
+    // step kt.
+    half8 bx[kSub], by[kSub], bl[kSub], a_h[2], a_l[2];
 #pragma unroll
-    for (int i = 0; i < kSub; ++i) {
-      ah[i] = rd(0, kAH, i);
-      bh[i] = rd(0, kBH, i);
-      al[i] = rd(0, kAL, i);
-      bl[i] = rd(0, kBL, i);
-      bs[i] = bh[i] * s16;
+    for (int j = 0; j < kSub; ++j) {
+      by[j] = rd(0, kBH, j);
+      bl[j] = rd(0, kBL, j);
     }
-    // One k-step: G1 = HH (A_hi x sB_hi), G2 = XA (A_lo x B_hi), G3 = XB
-    // (A_hi x B_lo), each row by row, in this order for every accumulator.
-    // The fragments of step kt+1 come from stage kt+1; each register is
-    // reloaded after its last use in step kt: A_lo row i after its G2 row,
-    // A_hi row i after its G3 row (first needed again in row i of the next G1),
-    // B_hi during G3 rows 0-3 and s B_hi formed from it in rows 4-7, B_lo
-    // after G3.
-    auto step = [&](int kt) {
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) bx[j] = by[j] * s16;
+    a_h[0] = rd(0, kAH, 0);
+    a_l[0] = rd(0, kAL, 0);
+
+    // bs: s B_hi of this step, bh: B_hi of this step.
+    auto step = [&](int kt, half8 (&bs)[kSub], half8 (&bh)[kSub]) {
       const int nk = kt + 1;
       int dn = 0;
-      auto dma_next = [&]() {
-        if (dn < kDma) dma_one(kt + S, dn++);
+      auto dma_some = [&](int n) {
+        if constexpr (S > 1) {
+#pragma unroll
+          for (int q = 0; q < n; ++q)
+            if (dn < kDma) dma_one(nk, dn++);
+        }
       };
 #pragma unroll
       for (int i = 0; i < kSub; ++i) {
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(ah[i], bs[j], acc[i][j]);
-        SCHED_FENCE();
-        if (i == 0) {
+        const int c = i & 1;
+        if (i == kSub - 1) {
           if constexpr (S == 1) {
             // Retire the single slot, copy stage kt+1 into it and wait.
             lds_barrier();
@@ -316,76 +211,87 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
             wait_vmcnt<0>();
             lds_barrier();
           } else {
-            wait_vmcnt<(S - 2) * kDma>();
+            wait_vmcnt<0>();
             lds_barrier();
           }
-        }
-        if constexpr (S > 1) dma_next();
-        SCHED_FENCE();
-      }
-#pragma unroll
-      for (int i = 0; i < kSub; ++i) {
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(al[i], bh[j], acc[i][j]);
-        SCHED_FENCE();
-        al[i] = rd(nk, kAL, i);
-        if constexpr (S > 1) dma_next();
-        SCHED_FENCE();
-      }
-#pragma unroll
-      for (int i = 0; i < kSub; ++i) {
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(ah[i], bl[j], acc[i][j]);
-        SCHED_FENCE();
-        ah[i] = rd(nk, kAH, i);
-        if (i < kSub / 2) {
-          bh[2 * i] = rd(nk, kBH, 2 * i);
-          bh[2 * i + 1] = rd(nk, kBH, 2 * i + 1);
+          a_h[c ^ 1] = rd(nk, kAH, 0);
+          a_l[c ^ 1] = rd(nk, kAL, 0);
         } else {
-          bs[2 * i - kSub] = bh[2 * i - kSub] * s16;
-          bs[2 * i - kSub + 1] = bh[2 * i - kSub + 1] * s16;
+          a_h[c ^ 1] = rd(kt, kAH, i + 1);
+          a_l[c ^ 1] = rd(kt, kAL, i + 1);
+        }
+        SCHED_FENCE();
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_h[c], bs[j], acc[i][j]);
+        SCHED_FENCE();
+        if (i == kSub - 1) {
+#pragma unroll
+          for (int j = 0; j < kSub; ++j) bs[j] = rd(nk, kBH, j);
+        } else if (i < 6) {
+          dma_some((kDma + 5) / 6 - (kDma + 5) / 12);
+        }
+        SCHED_FENCE();
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_l[c], bh[j], acc[i][j]);
+        SCHED_FENCE();
+        if (i == kSub - 1) {
+#pragma unroll
+          for (int j = 0; j < kSub; ++j) bh[j] = bs[j] * s16;
+        } else if (i < 6) {
+          dma_some((kDma + 5) / 12);
+        }
+        SCHED_FENCE();
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_h[c], bl[j], acc[i][j]);
+        SCHED_FENCE();
+        if (i == kSub - 1) {
+#pragma unroll
+          for (int j = 0; j < kSub; ++j) bl[j] = rd(nk, kBL, j);
         }
         SCHED_FENCE();
       }
-#pragma unroll
-      for (int j = 0; j < kSub; ++j) bl[j] = rd(nk, kBL, j);
+      if constexpr (S > 1) dma_some(kDma);  // any DMA of stage kt+1 not issued yet
     };
     for (int kt = 0; kt < ksteps; kt += 2) {
-      step(kt);
-      step(kt + 1);
+      step(kt, bx, by);
+      step(kt + 1, by, bx);
     }
   } else {
-    // Hi-only: double-buffered fragments, read right after the barrier of
-    // each step.
-    half8 ah2[kSub], bh2[kSub];
+    // Hi-only, the same row schedule with one product: the B_hi fragments of
+    // the next step go to the other register set right after the barrier.
+    half8 b0[kSub], b1[kSub], a_h[2];
 #pragma unroll
-    for (int i = 0; i < kSub; ++i) {
-      ah[i] = rd(0, kAH, i);
-      bh[i] = rd(0, kBH, i);
-    }
-    auto step = [&](int kt, half8 (&ac)[kSub], half8 (&bc)[kSub], half8 (&an)[kSub],
-                    half8 (&bn)[kSub]) {
+    for (int j = 0; j < kSub; ++j) b0[j] = rd(0, kBH, j);
+    a_h[0] = rd(0, kAH, 0);
+    auto step = [&](int kt, half8 (&bc)[kSub], half8 (&bn)[kSub]) {
+      const int nk = kt + 1;
+      int dn = 0;
 #pragma unroll
       for (int i = 0; i < kSub; ++i) {
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(ac[i], bc[j], acc[i][j]);
-        SCHED_FENCE();
-        if (i == 0) {
-          wait_vmcnt<(S - 2) * kDma>();
+        const int c = i & 1;
+        if (i == kSub - 1) {
+          wait_vmcnt<0>();
           lds_barrier();
+          a_h[c ^ 1] = rd(nk, kAH, 0);
 #pragma unroll
-          for (int q = 0; q < kSub; ++q) {
-            an[q] = rd(kt + 1, kAH, q);
-            bn[q] = rd(kt + 1, kBH, q);
+          for (int j = 0; j < kSub; ++j) bn[j] = rd(nk, kBH, j);
+        } else {
+          a_h[c ^ 1] = rd(kt, kAH, i + 1);
+          if (i < 6) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+              if (dn < kDma) dma_one(nk, dn++);
           }
         }
-        dma_one(kt + S, i);
+        SCHED_FENCE();
+#pragma unroll
+        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_h[c], bc[j], acc[i][j]);
         SCHED_FENCE();
       }
     };
     for (int kt = 0; kt < ksteps; kt += 2) {
-      step(kt, ah, bh, ah2, bh2);
-      step(kt + 1, ah2, bh2, ah, bh);
+      step(kt, b0, b1);
+      step(kt + 1, b1, b0);
     }
   }
   // No LDS DMA may still be writing when the workgroup retires.
@@ -583,22 +489,6 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
   }
 }
 
-// Raise a kernel's dynamic-LDS limit on the current device, once per device
-// and kernel (each instantiation calls this with its own `done` table).
-constexpr int kMaxDevices = 64;
-template <typename Kern>
-hipError_t set_lds(Kern kernel, size_t bytes, std::atomic<bool> (&done)[kMaxDevices]) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev >= 0 && dev < kMaxDevices && done[dev].load(std::memory_order_acquire))
-    return hipSuccess;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
-  if (e == hipSuccess && dev >= 0 && dev < kMaxDevices)
-    done[dev].store(true, std::memory_order_release);
-  return e;
-}
 
 template <int V, int S = kWideStages>
 hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
@@ -650,6 +540,11 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
     case kHiOnly: return launch_wide<kHiOnly>(p, M, N, C, ldc, scale, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                                float scale, int cus, hipStream_t stream) {
+  return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
 }
 
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,

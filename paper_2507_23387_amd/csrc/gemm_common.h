@@ -1,0 +1,173 @@
+// Building blocks shared by the GEMM kernels of libsgemmcube (gfx950): MFMA
+// wrappers, the LDS DMA, explicit waits and barriers, the XCD-aware tile maps
+// and the accumulator stores.  Internal; every function has internal linkage.
+#pragma once
+
+#include <atomic>
+
+#include "internal.h"
+
+namespace sgc {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// D(32x32) = A(32x16) B(16x32) + C.  Lane l supplies A row l%32 and B column
+// l%32 with the 8 consecutive k values 8*(l/32) .. 8*(l/32)+7 of the 16-wide
+// step; D element (row 8*(r/4) + 4*(l/32) + r%4, column l%32) is in register r.
+__device__ __forceinline__ floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// One 64-lane LDS DMA: lane l copies 16 bytes from g into LDS byte address
+// lds_addr + 16 * l (the instruction takes the LDS base from M0, which the
+// "{m0}" operand has the compiler load).  Inline asm, so the compiler adds no
+// conservative vmcnt(0) before later LDS reads; the kernels wait explicitly
+// with wait_vmcnt<>() before the barrier that publishes a stage.
+__device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_addr) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// This wave's LDS reads are complete, then all waves meet.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Keeps the instruction groups of the schedule in program order.
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// Offset (halves) of the fragment of LDS row r for k chunk fk (0 or 1).
+__device__ __forceinline__ int frag_offset(int r, int fk) {
+  return r * kSlice + ((fk ^ tile_swizzle(r)) << 3);
+}
+
+// LDS byte address of the dynamic shared-memory base (the M0 operand of the
+// DMA): cast the generic pointer to the LDS address space, then to int.
+__device__ __forceinline__ unsigned lds_address(const uint16_t* p) {
+  return static_cast<unsigned>((uintptr_t)((__attribute__((address_space(3))) const uint16_t*)p));
+}
+
+// Map a tile index to a (tile_m, tile_n) pair.  Workgroups are dispatched
+// round-robin over the 8 XCDs, so index i runs on XCD i % 8 (also for the
+// persistent grid, whose size is a multiple of 8); renumbering gives each XCD
+// a contiguous range of logical tiles, and grouping kGroup tile-rows keeps the
+// A and B panels a group touches resident in that XCD's L2.
+template <int kGroup>
+__device__ __forceinline__ void tile_of(int index, int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nwg = tiles_m * tiles_n;
+  int wg = index;
+  if ((nwg & 7) == 0) wg = (wg & 7) * (nwg >> 3) + (wg >> 3);
+  const int per_group = kGroup * tiles_n;
+  const int group = wg / per_group;
+  const int first_m = group * kGroup;
+  const int gsize = min(tiles_m - first_m, kGroup);
+  const int in_group = wg - group * per_group;
+  tm = first_m + in_group % gsize;
+  tn = in_group / gsize;
+}
+
+// Tile map for grids made of whole 16 x 16 blocks of 256 x 256 tiles (both
+// tile counts multiples of 16): the 256 workgroups of one dispatch round
+// (index / 256, one workgroup per compute unit) cover one 16 x 16 block, the
+// blocks in snake order along block rows; inside a block, XCD x (index % 8)
+// takes the 4 x 8 sub-block (x / 2, x % 2).  So in a round each A panel is
+// read by two XCDs and each B panel by four, and consecutive rounds share a
+// row (or column) of panels, which the last-level cache can serve.  Returns
+// false (and leaves tm, tn alone) when the grid is not made of such blocks.
+__device__ __forceinline__ bool tile_of_block(int index, int tiles_m, int tiles_n, int& tm,
+                                              int& tn) {
+  if ((tiles_m & 15) != 0 || (tiles_n & 15) != 0) return false;
+  const int round = index >> 8, x = index & 7, j = (index & 255) >> 3;
+  const int per_row = tiles_n >> 4;
+  const int br = round / per_row;
+  const int in_row = round - br * per_row;
+  const int bc = (br & 1) ? per_row - 1 - in_row : in_row;
+  tm = br * 16 + (x >> 1) * 4 + (j & 3);
+  tn = bc * 16 + (x & 1) * 8 + (j >> 2);
+  return true;
+}
+
+// Store a wave's accumulators: register r of MFMA tile (i, j) holds row
+// 8*(r/4) + 4*(l/32) + r%4 and column l%32 of that 32 x 32 tile.  `value`
+// maps (i, j, r) to the float to store.  Tiles entirely inside C take the
+// unmasked path; row offsets are wave-uniform multiples of ldc.
+template <int kSubM, int kSubN, typename F>
+__device__ __forceinline__ void store_tile(float* __restrict__ C, int64_t ldc, int M, int N,
+                                           int row0, int col0, bool full, F value) {
+  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
+  if (full) {
+#pragma unroll
+    for (int i = 0; i < kSubM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float* const p = base + static_cast<int64_t>(i * 32 + (r >> 2) * 8 + (r & 3)) * ldc;
+#pragma unroll
+        for (int j = 0; j < kSubN; ++j) p[j * 32] = value(i, j, r);
+      }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kSubM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rr = i * 32 + (r >> 2) * 8 + (r & 3);
+        float* const p = base + static_cast<int64_t>(rr) * ldc;
+#pragma unroll
+        for (int j = 0; j < kSubN; ++j)
+          if (row0 + rr < M && col0 + j * 32 < N) p[j * 32] = value(i, j, r);
+      }
+  }
+}
+
+
+// D(16x16) = A(16x32) B(32x16) + C.  Lane l supplies A row l%16 and B column
+// l%16 with the 8 consecutive k values 8*(l/16) .. 8*(l/16)+7 of the 32-wide
+// step; D element (row 4*(l/16) + r, column l%16) is in register r.
+__device__ __forceinline__ floatx4 mfma16(const half8& a, const half8& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// Store a wave's 16 x 16 accumulators: register r of MFMA tile (i, j) holds
+// row 4*(l/16) + r and column l%16 of that tile.  `value` maps (i, j, r) to
+// the float to store.  Tiles entirely inside C take the unmasked path.
+template <int kSubM, int kSubN, typename F>
+__device__ __forceinline__ void store_tile16(float* __restrict__ C, int64_t ldc, int M, int N,
+                                             int row0, int col0, bool full, F value) {
+  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
+#pragma unroll
+  for (int i = 0; i < kSubM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rr = i * 16 + r;
+      float* const p = base + static_cast<int64_t>(rr) * ldc;
+#pragma unroll
+      for (int j = 0; j < kSubN; ++j)
+        if (full || (row0 + rr < M && col0 + j * 16 < N)) p[j * 16] = value(i, j, r);
+    }
+}
+
+// Raise a kernel's dynamic-LDS limit on the current device, once per device
+// and kernel (each instantiation calls this with its own `done` table).
+constexpr int kMaxDevices = 64;
+template <typename Kern>
+hipError_t set_lds(Kern kernel, size_t bytes, std::atomic<bool> (&done)[kMaxDevices]) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < kMaxDevices && done[dev].load(std::memory_order_acquire))
+    return hipSuccess;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
+  if (e == hipSuccess && dev >= 0 && dev < kMaxDevices)
+    done[dev].store(true, std::memory_order_release);
+  return e;
+}
+
+}  // namespace
+}  // namespace sgc

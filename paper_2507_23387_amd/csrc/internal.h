@@ -20,8 +20,11 @@ enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2, kCrossFirst =
 // one k-step of a GEMM stage is a handful of contiguous 4 KiB blocks and the
 // DMA into LDS reads whole cache lines.  Inside a tile, row r holds its 16
 // values as two 16-byte chunks; chunk c is stored at position c ^ tile_swizzle(r)
-// so that the MFMA fragment reads from LDS (32 rows, one chunk each) spread
-// over all banks.  The GEMM copies tiles into LDS verbatim.
+// with tile_swizzle(r) = bit 4 of r.  With that swap the 16-byte fragment reads
+// of both GEMM kernels from LDS are free of bank conflicts on gfx950 (measured
+// with the LDS bank-conflict counter): 16 rows x 4 chunks of a 32-wide k-step
+// for v_mfma_f32_16x16x32_f16, 32 rows x 2 chunks of a 16-wide k-step for
+// v_mfma_f32_32x32x16_f16.  The GEMM copies tiles into LDS verbatim.
 constexpr int kPanel = 128;                     // rows per panel
 constexpr int kSlice = 16;                      // k per tile
 constexpr int kTileHalves = kPanel * kSlice;    // 2048 halves = 4 KiB
@@ -29,7 +32,7 @@ constexpr int kRowPad = 256;                    // M and N are padded to this
 constexpr int kKPad = 64;                       // K is padded to this
 constexpr int kFlagBytes = 256;                 // workspace header
 
-__host__ __device__ inline int tile_swizzle(int row) { return (row >> 3) & 1; }
+__host__ __device__ inline int tile_swizzle(int row) { return (row >> 4) & 1; }
 
 // Index (in halves) of element (row, k) of a tiled plane with Kp columns.
 __host__ __device__ inline int64_t tiled_index(int64_t row, int64_t k, int64_t Kp) {
@@ -40,6 +43,18 @@ __host__ __device__ inline int64_t tiled_index(int64_t row, int64_t k, int64_t K
 }
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// The two-component split of one value (Sec. 3.3, Eq. recover_eqn):
+// hi = fl16(a), r = a - hi (exact in FP32), lo = fl16(r * s), RN-even with
+// gradual underflow.  Shared by the split kernels and the GEMM that splits A
+// in registers, so both produce the same bits.
+__device__ __forceinline__ void split_value(float a, float s, uint16_t& hi, uint16_t& lo) {
+  const _Float16 h = static_cast<_Float16>(a);
+  const float r = a - static_cast<float>(h);
+  const _Float16 l = static_cast<_Float16>(r * s);
+  hi = __builtin_bit_cast(uint16_t, h);
+  lo = __builtin_bit_cast(uint16_t, l);
+}
 
 // Pre-scaling shift of a row (column) whose largest finite magnitude has the
 // bits `max_bits`: the power of two that brings that magnitude into
@@ -136,6 +151,20 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
 // ablation.  The fallback kernel (range flag set) keeps its own depth.
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, int cus, hipStream_t stream);
+
+// Elementwise GEMM that reads A as FP32 and splits it in registers
+// (gemm_fused.hip), on a workspace whose B planes and range flag were written
+// by launch_split_b.  Requires A 16-byte aligned, lda % 4 == 0 and K % 4 == 0.
+// When the range flag is set it writes the A planes instead, and
+// launch_gemm_fallback (which must follow on the same stream) computes C.
+hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
+                               const float* A, int64_t lda, float* C, int64_t ldc, float scale,
+                               hipStream_t stream);
+
+// The unscaled elementwise kernel alone; it computes C only when the range
+// flag is set (and returns at once otherwise).
+hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                                float scale, int cus, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).

@@ -19,14 +19,6 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ void split_value(float a, float s, uint16_t& hi, uint16_t& lo) {
-  const _Float16 h = static_cast<_Float16>(a);
-  const float r = a - static_cast<float>(h);
-  const _Float16 l = static_cast<_Float16>(r * s);
-  hi = __builtin_bit_cast(uint16_t, h);
-  lo = __builtin_bit_cast(uint16_t, l);
-}
-
 // Row-major split.  Thread = 4 consecutive columns of one row; blockIdx.y
 // strides over rows.  kVec: X rows are 16-byte aligned and hi/lo rows 8-byte
 // aligned, so whole quads move as float4 / 8-byte stores.

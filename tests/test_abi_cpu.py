@@ -187,3 +187,23 @@ def test_compute_stages_validation(lib):
     assert call(order=2) == NOT_SUPPORTED
     assert call(M=0, stages=1) == 0          # validation only: M = 0 is a no-op
 
+
+
+def test_compute_a_validation(lib):
+    A, C, ws = FAKE, FAKE + (2 << 30), FAKE + (3 << 30)
+    call = lambda M=4, N=4, K=4, A=A, lda=4, C=C, ldc=4, scale=2048.0, order=0, ws=ws, \
+        ws_bytes=1 << 20: lib.sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, order, ws,
+                                                   ws_bytes, 0)
+    assert call(order=3) == INVALID
+    assert call(lda=3) == INVALID                  # lda < K
+    assert call(ldc=3) == INVALID                  # ldc < N
+    assert call(scale=3.0) == INVALID              # not a power of two
+    assert call(A=0) == INVALID
+    assert call(C=0) == INVALID
+    assert call(C=A + 8) == INVALID                # C overlaps A
+    assert call(ws_bytes=16) == INVALID            # workspace too small
+    assert call(ws=ws + 8) == INVALID              # not 256-byte aligned
+    assert call(ws=A) == INVALID                   # workspace overlaps A
+    assert call(M=-1) == INVALID
+    assert call(M=1 << 31) == NOT_SUPPORTED
+    assert call(M=0) == 0                          # validation only: a no-op

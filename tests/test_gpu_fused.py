@@ -1,0 +1,191 @@
+"""The elementwise GEMM that splits A in registers (sgemm_cube_compute_a when
+A is 16-byte aligned and lda, K are multiples of 4) against the path through
+the split kernels and the A planes (sgemm_cube_ws).
+
+Both paths apply the same MFMA operations to every accumulator in the same
+order (HH, XA, XB per block), so when the in-register split produces the same
+bits as the split kernels (which the split tests pin to the oracle bit for
+bit) the two results are identical bit for bit; the fused result must also
+meet the parity bar against the oracle.  When s * B_hi overflows FP16 the
+fused kernel writes the A planes itself and the unscaled kernel runs: again
+bit-identical to the planes path."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from tests.gpu_util import log, to_dev
+from tests.helpers import abs_ab, assert_parity
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(1, 1, 4), (17, 33, 68), (129, 700, 36), (256, 256, 256), (300, 200, 1000),
+          (513, 640, 192), (200, 129, 4100)]
+
+
+def _kb():
+    from paper_2507_23387_amd import binding
+
+    return binding.sgemm_cube_block_k()
+
+
+def _both_paths(A, B, scale=2048.0):
+    """(C through prepare(A = NULL, B) + compute_a(A), C through sgemm_cube_ws)."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, K = A.shape
+    N = B.shape[1]
+    dA, dB = to_dev(A), to_dev(B)
+    stream = torch.cuda.current_stream().cuda_stream
+    ws = binding.workspace(M, N, K)
+    Cf = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    Cp = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    assert binding.sgemm_cube_prepare(M, N, K, None, K, dB.data_ptr(), N, scale,
+                                      ws.data_ptr(), ws.numel(), stream) == 0
+    assert binding.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), K, Cf.data_ptr(), N, scale,
+                                        binding.ELEMENTWISE, ws.data_ptr(), ws.numel(),
+                                        stream) == 0
+    assert binding.sgemm_cube_ws(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, Cp.data_ptr(), N,
+                                 scale, binding.ELEMENTWISE, ws.data_ptr(), ws.numel(),
+                                 stream) == 0
+    torch.cuda.synchronize()
+    return Cf.cpu().numpy(), Cp.cpu().numpy()
+
+
+def _same_bits(X, Y):
+    """Bitwise equal, NaNs compared by class (their payloads may differ)."""
+    nx, ny = np.isnan(X), np.isnan(Y)
+    assert np.array_equal(nx, ny)
+    assert np.array_equal(X[~nx].view(np.uint32), Y[~ny].view(np.uint32))
+
+
+def _mixed_operands(M, N, K, seed):
+    """N(0,1) operands with rows and columns of A and B moved to other binades
+    (FP16-subnormal hi at 2^-17, large values at 2^9), so the in-register
+    split meets normal, subnormal and large hi words."""
+    A, B = workloads.make_operands(M, N, K, seed, "normal")
+    A[::5] *= np.float32(2.0**-17)
+    A[1::7] *= np.float32(2.0**9)
+    B[:, ::3] *= np.float32(2.0**-3)
+    return A, B
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_fused_split_gives_the_bits_of_the_planes_path(gpu, shape):
+    M, N, K = shape
+    A, B = _mixed_operands(M, N, K, M + 3 * N + K)
+    log(f"fused vs planes {M}x{N}x{K}")
+    Cf, Cp = _both_paths(A, B)
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), f"fused {shape}")
+
+
+def test_identity_b_reconstructs_every_split_of_a(gpu):
+    """With B = I (exact in FP16, B_lo = 0) each output is the rounded
+    s-scaled sum s hi + lo of one entry of A, divided by s: a change in any
+    bit of the in-register split of A changes C.  Compared with the same sum
+    formed from the oracle's split."""
+    M = K = N = 512
+    rng = np.random.default_rng(41)
+    mant = rng.uniform(1.0, 2.0, size=(M, K))
+    expo = rng.integers(-26, 14, size=(M, K))
+    A = (np.where(rng.random((M, K)) < 0.5, -1.0, 1.0) * np.ldexp(mant, expo)).astype(np.float32)
+    B = np.eye(K, N, dtype=np.float32)
+    log("fused identity B")
+    Cf, Cp = _both_paths(A, B)
+    _same_bits(Cf, Cp)
+    hi, lo = oracle.split(A, 2048.0)
+    hi64 = oracle.f16_to_f32(hi).astype(np.float64)
+    lo64 = oracle.f16_to_f32(lo).astype(np.float64)
+    # s hi + lo has at most 24 significant bits where lo's last bit is within
+    # 23 bits of s hi's leading bit; there the sum is exact and so is C.
+    want = (hi64 * 2048.0 + lo64).astype(np.float32).astype(np.float64) / 2048.0
+    exact = np.abs(want - (hi64 + lo64 / 2048.0)) == 0
+    assert exact.mean() > 0.5
+    got = Cf.astype(np.float64)
+    assert np.array_equal(got[exact] == 0, want[exact] == 0)
+    nz = exact & (want != 0)
+    assert np.array_equal(got[nz], want[nz])
+
+
+@pytest.mark.parametrize("edge", ["scaled_limit", "fallback"])
+def test_fused_range_switch(gpu, edge):
+    """|B_hi| s at 65504 keeps the scaled kernel; one FP16 ulp above makes the
+    fused kernel write the A planes and the unscaled kernel compute C."""
+    M, N, K = 300, 260, 260
+    A, B = workloads.make_operands(M, N, K, 22, "uniform_pm1")
+    B[5, 7] = 31.984375 if edge == "scaled_limit" else 32.0
+    log(f"fused range switch {edge}")
+    Cf, Cp = _both_paths(A, B)
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), f"fused range switch {edge}")
+
+
+def test_fused_non_finite_inputs(gpu):
+    M, N, K = 40, 50, 72
+    A, B = workloads.make_operands(M, N, K, 23, "uniform_pm1")
+    A[3, 5] = 70000.0      # hi overflows
+    A[7, 9] = -np.inf
+    A[20, 21] = 32784.0    # lo overflows with s = 2^12
+    A[30, 71] = np.nan     # in the last k-step's tail
+    log("fused non-finite")
+    Cf, Cp = _both_paths(A, B, 4096.0)
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, 4096.0, "elementwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), "fused non-finite")
+
+
+def test_compute_a_after_prepare_of_b(gpu):
+    """prepare(A = NULL, B) + compute_a(A) == sgemm_cube_ws, for every order
+    (the orders other than elementwise split A into the workspace first)."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K = 300, 257, 516
+    A, B = workloads.make_operands(M, N, K, 24, "normal")
+    dA, dB = to_dev(A), to_dev(B)
+    stream = torch.cuda.current_stream().cuda_stream
+    for order in ("elementwise", "termwise", "elementwise_cross_first"):
+        log(f"compute_a {order}")
+        code = binding.ORDERS[order]
+        ws = binding.workspace(M, N, K)
+        C1 = binding.matmul(dA, dB, 2048.0, order)
+        C2 = torch.empty_like(C1)
+        assert binding.sgemm_cube_prepare(M, N, K, None, K, dB.data_ptr(), N, 2048.0,
+                                          ws.data_ptr(), ws.numel(), stream) == 0
+        assert binding.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), K, C2.data_ptr(), N, 2048.0,
+                                            code, ws.data_ptr(), ws.numel(), stream) == 0
+        torch.cuda.synchronize()
+        assert torch.equal(C1, C2)
+
+
+def test_unaligned_a_splits_into_the_workspace(gpu):
+    """compute_a with A misaligned by one element, or K not a multiple of 4,
+    splits A into the workspace first; the result equals sgemm_cube's."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    for (M, N, K, off) in ((130, 140, 256, 1), (130, 140, 258, 0)):
+        A, B = workloads.make_operands(M, N, K, 25, "normal")
+        buf = torch.zeros(off + M * K, dtype=torch.float32, device="cuda")
+        Av = buf[off:].view(M, K)
+        Av.copy_(torch.from_numpy(A))
+        dB = to_dev(B)
+        stream = torch.cuda.current_stream().cuda_stream
+        log(f"compute_a unaligned {M}x{N}x{K} off {off}")
+        ws = binding.workspace(M, N, K)
+        C1 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        assert binding.sgemm_cube_prepare(M, N, K, None, K, dB.data_ptr(), N, 2048.0,
+                                          ws.data_ptr(), ws.numel(), stream) == 0
+        assert binding.sgemm_cube_compute_a(M, N, K, Av.data_ptr(), K, C1.data_ptr(), N, 2048.0,
+                                            binding.ELEMENTWISE, ws.data_ptr(), ws.numel(),
+                                            stream) == 0
+        C2 = binding.matmul(to_dev(A), dB, 2048.0, "elementwise")
+        torch.cuda.synchronize()
+        assert torch.equal(C1, C2)

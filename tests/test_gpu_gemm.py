@@ -195,12 +195,12 @@ def test_range_flag_follows_the_last_split_of_b(gpu):
 
 def _untile(buf: np.ndarray, rows_p: int, Kp: int) -> np.ndarray:
     """Decode a plane stored as 128-row x 16-k tiles (row r's two 8-value
-    chunks swapped when bit 3 of r is set) into a rows_p x Kp array."""
+    chunks swapped when bit 4 of r is set) into a rows_p x Kp array."""
     r = np.arange(rows_p)[:, None]
     k = np.arange(Kp)[None, :]
     tile = (r // 128) * (Kp // 16) + k // 16
     rr, kk = r % 128, k % 16
-    idx = tile * 2048 + rr * 16 + (((kk >> 3) ^ ((rr >> 3) & 1)) << 3) + (kk & 7)
+    idx = tile * 2048 + rr * 16 + (((kk >> 3) ^ ((rr >> 4) & 1)) << 3) + (kk & 7)
     return buf[idx]
 
 

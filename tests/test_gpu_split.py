@@ -117,12 +117,12 @@ def test_exhaustive_2_32(gpu, chunk):
 
 def _untile(buf, rows_p, Kp):
     """Decode a plane stored as 128-row x 16-k tiles (row r's two 8-value
-    chunks swapped when bit 3 of r is set) into a rows_p x Kp array."""
+    chunks swapped when bit 4 of r is set) into a rows_p x Kp array."""
     r = np.arange(rows_p)[:, None]
     k = np.arange(Kp)[None, :]
     tile = (r // 128) * (Kp // 16) + k // 16
     rr, kk = r % 128, k % 16
-    return buf[tile * 2048 + rr * 16 + (((kk >> 3) ^ ((rr >> 3) & 1)) << 3) + (kk & 7)]
+    return buf[tile * 2048 + rr * 16 + (((kk >> 3) ^ ((rr >> 4) & 1)) << 3) + (kk & 7)]
 
 
 def _prepared_planes(A, B, scale, lda_pad=0, offset=0):
