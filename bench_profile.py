@@ -1,10 +1,10 @@
 """Summaries of rocprofv3 runs of bench.py, for the files under profiles/.
 
-    python bench_profile.py stats DIR [--title T] [--cmd C]
+    python bench_profile.py stats DIR
         kernel statistics of a `rocprofv3 --kernel-trace --stats` run
         (DIR/**/*kernel_stats.csv) as a markdown table
     python bench_profile.py traffic FETCH_DIR WRITE_DIR --workload W --order O
-                            [--copy-mib 512] [--cmd-fetch C] [--cmd-write C]
+                            [--copy-mib 512]
         HBM traffic of the GEMM kernel from two `rocprofv3 --pmc` passes
         (FETCH_SIZE, then WRITE_SIZE), each scaled by what the same counter
         reads for bench.py's plain device copy of --copy-mib MiB; writes the
@@ -50,10 +50,10 @@ def _rows(directory: str, suffix: str):
 
 def short(name: str) -> str:
     """Kernel name without the namespace and argument list."""
-    n = name.split("(")[0]
-    for pre in ("void ", "sgc::(anonymous namespace)::", "sgc::"):
+    n = name
+    for pre in ("void ", "(anonymous namespace)::", "sgc::"):
         n = n.replace(pre, "")
-    return n[:60]
+    return n.split("(")[0][:60]
 
 
 def stats(directory: str) -> str:
