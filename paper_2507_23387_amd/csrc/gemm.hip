@@ -63,47 +63,76 @@ static_assert(kKSteps == 1, "one MFMA k-step per slice");
 static_assert(kKPad % (2 * kSlice) == 0, "the main loops take two slices per iteration");
 
 // ---------------------------------------------------------------------------
-// 256 x 256 tiles: scaled elementwise and hi-only, on v_mfma_f32_16x16x32_f16.
+// 256 x 256 tiles on v_mfma_f32_16x16x32_f16: the scaled elementwise kernel
+// and the hi-only baseline.
 //
 // The 16 x 16 x 32 form is used here because under the board's power limit it
 // sustains a higher FP16 rate on random operands than the 32 x 32 x 16 form
 // (less energy per product, so a higher shader clock at the same power).
 constexpr int kWide = 256;
 constexpr int kWideThreads = 256;
-constexpr int kWideStages = 2;
-constexpr int kStep = 2 * kSlice;  // k per MFMA step of the wide kernel (32): two slices
+constexpr int kStep = 2 * kSlice;                  // k per MFMA step (32): two slices
+constexpr int kWSub = 8;                           // 16 x 16 MFMA tiles per wave side
+constexpr int kStepPlaneHalves = kWide * kStep;    // one plane of one step: 16 KiB
+constexpr int kSlotHalves = 2 * kStepPlaneHalves;  // hi and lo planes of one operand
+constexpr size_t kElLdsBytes = static_cast<size_t>(4) * kSlotHalves * 2;  // 128 KiB
+constexpr size_t kHiLdsBytes = static_cast<size_t>(2) * 2 * kStepPlaneHalves * 2;  // 64 KiB
 
-
-template <int V>
-constexpr int wide_planes() { return V == kElementwise ? 4 : 2; }
-
-template <int V, int S>
-constexpr size_t wide_lds_bytes() {
-  return static_cast<size_t>(S) * wide_planes<V>() * kWide * kStep * 2;
+// Fragment offsets (halves, within one plane of one step) of this lane for a
+// wave whose rows are panel `panel` of the tile: block i (rows 16 i .. 16 i
+// + 15 of the panel) is at off[i & 1] + 16 i * kSlice.  Lane l reads row
+// 16 i + l%16 and k chunk c = l/16 of the step, i.e. chunk c%2 of slice c/2;
+// the chunk swap of the tile layout depends on bit 4 of the row, i.e. on the
+// parity of i.
+__device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off)[2]) {
+  const int fr = lane & 15, fc = lane >> 4;
+#pragma unroll
+  for (int par = 0; par < 2; ++par)
+    off[par] = (2 * panel + (fc >> 1)) * kTileHalves + fr * kSlice +
+               (((fc & 1) ^ tile_swizzle(16 * par + fr)) << 3);
 }
 
-
-// S = number of LDS stage slots, one 32-k step each (64 KiB with four planes).
-// S = 2: the DMAs of stage kt+2 are in flight while step kt+1 computes.
-// S = 1 (no prefetch, for the pipeline ablation): the next stage is copied and
-// waited for inside each step.
-template <int V, int S>
-__global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
+// Scaled elementwise kernel (Eq. elementwise, Sec. 4.5), one 256 x 256 tile
+// of C per workgroup, 4 waves of 128 x 128 (one per SIMD; 64 accumulators of
+// 16 x 16 in the 256 AGPRs).  The contraction is cut into blocks g of one
+// MFMA k-step (32), and the accumulator holds s * acc, so the three
+// per-block additions of the equation are three chained MFMAs:
+//   s*acc <- fl(s*acc + A_hi (s B_hi))   = s * fl(acc + HH_g)
+//   s*acc <- fl(s*acc + A_lo B_hi)       = s * fl(acc + XA_g / s)
+//   s*acc <- fl(s*acc + A_hi B_lo)       = s * fl(acc + XB_g / s)
+// and C = (s*acc) / s at the end.  s B_hi is formed in registers with
+// v_pk_mul_f16; it is exact because s is a power of two, provided
+// |B_hi| s <= 65504, which the split of B checks (the range flag; when it is
+// set this kernel returns at once and the narrow kernel computes C).  Each
+// block term is summed by the MFMA together with the accumulator, with one
+// rounding, instead of being rounded to FP32 on its own first.
+//
+// Data path.  LDS holds two A slots and two B slots (32 KiB each: the hi and
+// lo planes of one operand for one step, copied verbatim from the tiled planes
+// by LDS DMA).  A wave keeps the A fragments of the whole step in registers
+// (A_hi, A_lo of its 128 rows) and streams B one 16-column block at a time,
+// read from LDS one block ahead.  During step kt it
+//   - reads the A fragments of step kt+1 into a second register set, two or
+//     three per column block (blocks 0-6), the two sets swapping roles each
+//     step;
+//   - copies B stage kt+1 and A stage kt+2 into LDS with 16 DMAs issued in
+//     column blocks 0 and 1, so each has most of the step to land;
+// and every LDS read, DMA and VALU instruction sits between two MFMAs.  One
+// barrier per step, before the last column block, publishes B stage kt+1 and
+// A stage kt+2 and retires the slots of B stage kt and A stage kt+1.  Stages
+// past the end repeat the last stage, so every wait count is a constant.
+// kPrefetch = false (pipeline ablation): the 16 DMAs of a step are issued
+// right before its barrier, so no copy overlaps the MFMAs.
+template <bool kPrefetch>
+__global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
-  static_assert(V == kElementwise || V == kHiOnly, "wide kernel variants");
-  static_assert((S == 1 && V == kElementwise) || S == 2, "stage count");
-  constexpr bool kEl = V == kElementwise;
-  constexpr int kPlanes = wide_planes<V>();       // LDS slots: A_hi, B_hi, A_lo, B_lo
-  constexpr int kPlaneHalves = kWide * kStep;     // two panels x two slices: four tiles
-  constexpr int kStageHalves = kPlanes * kPlaneHalves;
-  constexpr int kDma = kPlanes * 4;               // 1 KiB DMAs per wave per stage
-  constexpr int kSub = 8;                         // 16 x 16 MFMA tiles per wave side
-  if constexpr (kEl) {
-    if (range[0] == range[1]) return;  // s B_hi overflows FP16: the narrow kernel runs instead
-  }
+  constexpr int kBBase = 2 * kSlotHalves;     // the B slots follow the two A slots
+  constexpr int kDmaCols = 2;                 // column blocks that issue the DMAs
+  constexpr int kDmaPerCol = 16 / kDmaCols;   // after MFMAs 2, 5, ..., 23 of a block
+  if (range[0] == range[1]) return;  // s B_hi overflows FP16: the narrow kernel runs instead
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
@@ -115,195 +144,226 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_wide_kernel(
   const int64_t slices = Kp / kSlice;
   const int ksteps = static_cast<int>(slices / 2);
 
-  // A stage holds, per plane, the tiles (panel ph, slice sl) of the tile's two
-  // panels and the step's two slices at tile position 2*ph + sl.  Wave w copies
-  // 1 KiB block w of each of those four tiles.
+  // One plane of one stage is the four 4 KiB tiles (panel ph, slice sl) of
+  // the tile's two panels and the step's two slices, at tile position
+  // 2*ph + sl of the slot; wave w copies 1 KiB block w of each.
   const int64_t panel_stride = slices * kTileHalves;
-  const uint16_t* src[4] = {a_hi + 2 * tm * panel_stride, b_hi + 2 * tn * panel_stride,
-                            kEl ? a_lo + 2 * tm * panel_stride : nullptr,
-                            kEl ? b_lo + 2 * tn * panel_stride : nullptr};
-  const int64_t lane_off = w * 512 + lane * 8;
-  const unsigned lds_base = lds_address(lds);
-  auto dma_one = [&](int kt, int n) {  // n-th DMA of stage kt, n < kDma
-    const int ktc = min(kt, ksteps - 1);
+  const unsigned lane_off = static_cast<unsigned>(w * 512 + lane * 8) * 2;  // bytes
+  const uint16_t* const src_a[2] = {a_hi + 2 * tm * panel_stride, a_lo + 2 * tm * panel_stride};
+  const uint16_t* const src_b[2] = {b_hi + 2 * tn * panel_stride, b_lo + 2 * tn * panel_stride};
+  const unsigned lds_base = lds_address(lds) + w * 1024;
+  // n-th DMA (n < 8) of the A or B stage t.
+  auto dma_stage = [&](const uint16_t* const (&src)[2], int base, int t, int n) {
+    const int tc = min(t, ksteps - 1);
     const int p = n >> 2, ph = (n >> 1) & 1, sl = n & 1;
-    const unsigned dst = lds_base + ((kt % S) * kStageHalves + p * kPlaneHalves +
-                                     (2 * ph + sl) * kTileHalves + w * 512) * 2;
-    dma16(src[p] + ph * panel_stride + static_cast<int64_t>(2 * ktc + sl) * kTileHalves +
-              lane_off, dst);
+    dma16s(src[p] + ph * panel_stride + static_cast<int64_t>(2 * tc + sl) * kTileHalves,
+           lane_off,
+           lds_base + (base + (t & 1) * kSlotHalves + p * kStepPlaneHalves +
+                       (2 * ph + sl) * kTileHalves) * 2);
+  };
+  // The d-th of the 16 DMAs of step kt: B stage kt+1, then A stage kt+2.
+  auto dma = [&](int kt, int d) {
+    if (d < 8)
+      dma_stage(src_b, kBBase, kt + 1, d);
+    else
+      dma_stage(src_a, 0, kt + 2, d - 8);
   };
 
-  // Fragment of block i (rows 16 i .. 16 i + 15 of this wave's 128 rows, which
-  // are panel wm of A / panel wn of B): lane l reads row 16 i + l%16, k chunk
-  // c = l/16 of the step, i.e. chunk c%2 of slice c/2.  The chunk swap of the
-  // tile layout depends on bit 4 of the row, i.e. on the parity of i.
-  const int fr = lane & 15, fc = lane >> 4;
   int a_off[2], b_off[2];
-#pragma unroll
-  for (int par = 0; par < 2; ++par) {
-    const int row_off = fr * kSlice + (((fc & 1) ^ tile_swizzle(16 * par + fr)) << 3);
-    a_off[par] = (2 * wm + (fc >> 1)) * kTileHalves + row_off;
-    b_off[par] = (2 * wn + (fc >> 1)) * kTileHalves + row_off;
-  }
-  constexpr int kAH = 0, kBH = 1, kAL = 2, kBL = 3;
-  auto rd = [&](int kt, int plane, int i) -> half8 {
-    const int off = (plane == kAH || plane == kAL) ? a_off[i & 1] : b_off[i & 1];
-    return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + plane * kPlaneHalves +
-                                           off + i * 16 * kSlice);
+  wide_frag_offsets(lane, wm, a_off);
+  wide_frag_offsets(lane, wn, b_off);
+  auto rd_a = [&](int t, int p, int i) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + (t & 1) * kSlotHalves + p * kStepPlaneHalves +
+                                           a_off[i & 1] + i * 16 * kSlice);
   };
-  const _Float16 s16 = static_cast<_Float16>(s);
+  auto rd_b = [&](int t, int p, int j) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + kBBase + (t & 1) * kSlotHalves +
+                                           p * kStepPlaneHalves + b_off[j & 1] + j * 16 * kSlice);
+  };
+  // (s, s) as a packed FP16 pair, wave-uniform.
+  const uint16_t s_bits = __builtin_bit_cast(uint16_t, static_cast<_Float16>(s));
+  const uint32_t s2 = static_cast<uint32_t>(
+      __builtin_amdgcn_readfirstlane(static_cast<int>(s_bits * 0x10001u)));
 
-  floatx4 acc[kSub][kSub];
+  floatx4 acc[kWSub][kWSub];
 #pragma unroll
-  for (int i = 0; i < kSub; ++i)
+  for (int i = 0; i < kWSub; ++i)
 #pragma unroll
-    for (int j = 0; j < kSub; ++j) acc[i][j] = floatx4{};
+    for (int j = 0; j < kWSub; ++j) acc[i][j] = floatx4{};
 
-  // Prologue: stage 0 (each step copies the next stage).
-#pragma unroll
-  for (int n = 0; n < kDma; ++n) dma_one(0, n);
+  // Prologue: A stages 0 and 1 and B stage 0; A stage 0 goes to registers.
+  static_for<8>([&](auto n) { dma_stage(src_a, 0, 0, decltype(n)::value); });
+  static_for<8>([&](auto n) { dma_stage(src_a, 0, 1, decltype(n)::value); });
+  static_for<8>([&](auto n) { dma_stage(src_b, kBBase, 0, decltype(n)::value); });
   wait_vmcnt<0>();
   lds_barrier();
+  // (AH, AL) and (NH, NL): A_hi, A_lo of the current and of the next step.
+  // bh, bl, bs: B_hi, B_lo, s B_hi of a column block, double-buffered by the
+  // parity of the block.
+  half8 AH[kWSub], AL[kWSub], NH[kWSub], NL[kWSub], bh[2], bl[2], bs[2];
+#pragma unroll
+  for (int i = 0; i < kWSub; ++i) {
+    AH[i] = rd_a(0, 0, i);
+    AL[i] = rd_a(0, 1, i);
+  }
+  bh[0] = rd_b(0, 0, 0);
+  bl[0] = rd_b(0, 1, 0);
+  bs[0] = pk_scale(bh[0], s2);
+  lds_barrier();  // A slot 0 is refilled (stage 2) during step 0
 
-  if constexpr (kEl) {
-    // Row-fused schedule: for each row i of 16 x 16 blocks the wave issues
-    // HH(i, .), then XA(i, .), then XB(i, .), so every accumulator still sees
-    // the block terms in the order HH, XA, XB.  The B fragments of the whole
-    // step stay in registers (s B_hi, B_hi, B_lo); A fragments are needed one
-    // row at a time and are read one row ahead.  The two B_hi register sets
-    // swap roles every step: after HH of row 7 the set that held s B_hi
-    // receives the next step's B_hi, and after XA of row 7 the other set
-    // receives s times it.  One barrier per step, before row 7, publishes
-    // stage kt+1 (row 7 reads the next step's fragments from it) and retires
-    // the slot of stage kt; the DMAs of stage kt+1 are issued in rows 0-5 of
-    // step kt.
-    half8 bx[kSub], by[kSub], bl[kSub], a_h[2], a_l[2];
-#pragma unroll
-    for (int j = 0; j < kSub; ++j) {
-      by[j] = rd(0, kBH, j);
-      bl[j] = rd(0, kBL, j);
-    }
-#pragma unroll
-    for (int j = 0; j < kSub; ++j) bx[j] = by[j] * s16;
-    a_h[0] = rd(0, kAH, 0);
-    a_l[0] = rd(0, kAL, 0);
-
-    // bs: s B_hi of this step, bh: B_hi of this step.
-    auto step = [&](int kt, half8 (&bs)[kSub], half8 (&bh)[kSub]) {
-      const int nk = kt + 1;
-      int dn = 0;
-      auto dma_some = [&](int n) {
-        if constexpr (S > 1) {
-#pragma unroll
-          for (int q = 0; q < n; ++q)
-            if (dn < kDma) dma_one(nk, dn++);
-        }
-      };
-#pragma unroll
-      for (int i = 0; i < kSub; ++i) {
-        const int c = i & 1;
-        if (i == kSub - 1) {
-          if constexpr (S == 1) {
-            // Retire the single slot, copy stage kt+1 into it and wait.
-            lds_barrier();
-#pragma unroll
-            for (int n = 0; n < kDma; ++n) dma_one(nk, n);
-            wait_vmcnt<0>();
-            lds_barrier();
-          } else {
-            wait_vmcnt<0>();
-            lds_barrier();
-          }
-          a_h[c ^ 1] = rd(nk, kAH, 0);
-          a_l[c ^ 1] = rd(nk, kAL, 0);
-        } else {
-          a_h[c ^ 1] = rd(kt, kAH, i + 1);
-          a_l[c ^ 1] = rd(kt, kAL, i + 1);
-        }
-        SCHED_FENCE();
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_h[c], bs[j], acc[i][j]);
-        SCHED_FENCE();
-        if (i == kSub - 1) {
-#pragma unroll
-          for (int j = 0; j < kSub; ++j) bs[j] = rd(nk, kBH, j);
-        } else if (i < 6) {
-          dma_some((kDma + 5) / 6 - (kDma + 5) / 12);
-        }
-        SCHED_FENCE();
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_l[c], bh[j], acc[i][j]);
-        SCHED_FENCE();
-        if (i == kSub - 1) {
-#pragma unroll
-          for (int j = 0; j < kSub; ++j) bh[j] = bs[j] * s16;
-        } else if (i < 6) {
-          dma_some((kDma + 5) / 12);
-        }
-        SCHED_FENCE();
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_h[c], bl[j], acc[i][j]);
-        SCHED_FENCE();
-        if (i == kSub - 1) {
-#pragma unroll
-          for (int j = 0; j < kSub; ++j) bl[j] = rd(nk, kBL, j);
-        }
-        SCHED_FENCE();
+  // One step.  Column block j issues HH(., j), XA(., j), XB(., j), so every
+  // accumulator sees the block terms in the order HH, XA, XB, and the three
+  // MFMAs of one accumulator are 8 MFMAs apart.  After MFMA m of a block:
+  // m = 1, 9, 17 read the next A fragments, m = 2, 5, ..., 23 of blocks 0-1
+  // issue the DMAs, m = 14 forms the next block's s B_hi.
+  auto step = [&](int kt, half8 (&ah)[kWSub], half8 (&al)[kWSub], half8 (&nh)[kWSub],
+                  half8 (&nl)[kWSub]) {
+    static_for<kWSub>([&](auto J) {
+      constexpr int j = decltype(J)::value, c = j & 1;
+      if constexpr (j == kWSub - 1) {
+        if constexpr (!kPrefetch) static_for<16>([&](auto d) { dma(kt, decltype(d)::value); });
+        wait_vmcnt<0>();
+        lds_barrier();
+        bh[c ^ 1] = rd_b(kt + 1, 0, 0);
+        bl[c ^ 1] = rd_b(kt + 1, 1, 0);
+      } else {
+        bh[c ^ 1] = rd_b(kt, 0, j + 1);
+        bl[c ^ 1] = rd_b(kt, 1, j + 1);
       }
-      if constexpr (S > 1) dma_some(kDma);  // any DMA of stage kt+1 not issued yet
-    };
-    for (int kt = 0; kt < ksteps; kt += 2) {
-      step(kt, bx, by);
-      step(kt + 1, by, bx);
-    }
-  } else {
-    // Hi-only, the same row schedule with one product: the B_hi fragments of
-    // the next step go to the other register set right after the barrier.
-    half8 b0[kSub], b1[kSub], a_h[2];
-#pragma unroll
-    for (int j = 0; j < kSub; ++j) b0[j] = rd(0, kBH, j);
-    a_h[0] = rd(0, kAH, 0);
-    auto step = [&](int kt, half8 (&bc)[kSub], half8 (&bn)[kSub]) {
-      const int nk = kt + 1;
-      int dn = 0;
-#pragma unroll
-      for (int i = 0; i < kSub; ++i) {
-        const int c = i & 1;
-        if (i == kSub - 1) {
-          wait_vmcnt<0>();
-          lds_barrier();
-          a_h[c ^ 1] = rd(nk, kAH, 0);
-#pragma unroll
-          for (int j = 0; j < kSub; ++j) bn[j] = rd(nk, kBH, j);
-        } else {
-          a_h[c ^ 1] = rd(kt, kAH, i + 1);
-          if (i < 6) {
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-              if (dn < kDma) dma_one(nk, dn++);
+      SCHED_FENCE();
+      // A fragments rb .. re-1 of the 16 (A_hi rows 0-7, then A_lo) in block j.
+      constexpr int rb = (16 * j + 6) / 7, re = (16 * (j + 1) + 6) / 7;
+      static_for<3 * kWSub>([&](auto Mc) {
+        constexpr int m = decltype(Mc)::value, g = m / kWSub, i = m % kWSub;
+        if constexpr (g == 0)
+          mfma16_acc(acc[i][j], ah[i], bs[c]);
+        else if constexpr (g == 1)
+          mfma16_acc(acc[i][j], al[i], bh[c]);
+        else
+          mfma16_acc(acc[i][j], ah[i], bl[c]);
+        SCHED_FENCE();
+        if constexpr (m == 14) bs[c ^ 1] = pk_scale(bh[c ^ 1], s2);
+        if constexpr (j < kWSub - 1 && m % kWSub == 1) {
+          constexpr int r = rb + m / kWSub;
+          if constexpr (r < re) {
+            if constexpr (r < kWSub)
+              nh[r] = rd_a(kt + 1, 0, r);
+            else
+              nl[r - kWSub] = rd_a(kt + 1, 1, r - kWSub);
           }
         }
+        if constexpr (kPrefetch && j < kDmaCols && m % 3 == 2) dma(kt, j * kDmaPerCol + m / 3);
         SCHED_FENCE();
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) acc[i][j] = mfma16(a_h[c], bc[j], acc[i][j]);
-        SCHED_FENCE();
-      }
-    };
-    for (int kt = 0; kt < ksteps; kt += 2) {
-      step(kt, b0, b1);
-      step(kt + 1, b1, b0);
-    }
+      });
+    });
+  };
+  for (int kt = 0; kt < ksteps; kt += 2) {
+    step(kt, AH, AL, NH, NL);
+    step(kt + 1, NH, NL, AH, AL);
   }
   // No LDS DMA may still be writing when the workgroup retires.
   wait_vmcnt<0>();
+  mfma_drain();
 
-  const float out_scale = kEl ? inv_s : 1.0f;
   const int col0 = tn * kWide + wn * 128 + (lane & 15);
   const int row0 = tm * kWide + wm * 128 + (lane >> 4) * 4;
   const bool full = (tm + 1) * kWide <= M && (tn + 1) * kWide <= N;
-  store_tile16<kSub, kSub>(C, ldc, M, N, row0, col0, full,
-                           [&](int i, int j, int r) { return acc[i][j][r] * out_scale; });
+  store_tile16<kWSub, kWSub>(C, ldc, M, N, row0, col0, full,
+                             [&](int i, int j, int r) { return acc[i][j][r] * inv_s; });
 }
+
+// Hi-only kernel: C = A_hi B_hi, the native-FP16 GEMM baseline (Sec. 6.2),
+// with the tile, wave split and LDS layout of the elementwise kernel minus
+// the lo planes: a two-slot ring of (A_hi, B_hi) stages; each wave walks its
+// rows of 16 x 16 blocks, B fragments of the step in registers, A fragments
+// read one row ahead; one barrier per step publishes stage kt+1.
+__global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
+    const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ b_hi, int Kp, int tiles_m,
+    int tiles_n, float* __restrict__ C, int64_t ldc, int M, int N) {
+  constexpr int kStageHalves = 2 * kStepPlaneHalves;  // A_hi, B_hi
+  constexpr int kDma = 8;                             // 1 KiB DMAs per wave per stage
+  extern __shared__ __align__(16) uint16_t lds[];
+
+  int tm, tn;
+  if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn))
+    tile_of<4>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  const int64_t slices = Kp / kSlice;
+  const int ksteps = static_cast<int>(slices / 2);
+  const int64_t panel_stride = slices * kTileHalves;
+  const unsigned lane_off = static_cast<unsigned>(w * 512 + lane * 8) * 2;
+  const uint16_t* const src[2] = {a_hi + 2 * tm * panel_stride, b_hi + 2 * tn * panel_stride};
+  const unsigned lds_base = lds_address(lds) + w * 1024;
+  auto dma_one = [&](int kt, int n) {  // n-th DMA of stage kt, n < kDma
+    const int ktc = min(kt, ksteps - 1);
+    const int p = n >> 2, ph = (n >> 1) & 1, sl = n & 1;
+    dma16s(src[p] + ph * panel_stride + static_cast<int64_t>(2 * ktc + sl) * kTileHalves,
+           lane_off,
+           lds_base + ((kt & 1) * kStageHalves + p * kStepPlaneHalves +
+                       (2 * ph + sl) * kTileHalves) * 2);
+  };
+  int a_off[2], b_off[2];
+  wide_frag_offsets(lane, wm, a_off);
+  wide_frag_offsets(lane, wn, b_off);
+  auto rd = [&](int kt, int p, int i) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + (kt & 1) * kStageHalves + p * kStepPlaneHalves +
+                                           (p == 0 ? a_off[i & 1] : b_off[i & 1]) +
+                                           i * 16 * kSlice);
+  };
+
+  floatx4 acc[kWSub][kWSub];
+#pragma unroll
+  for (int i = 0; i < kWSub; ++i)
+#pragma unroll
+    for (int j = 0; j < kWSub; ++j) acc[i][j] = floatx4{};
+
+  static_for<kDma>([&](auto n) { dma_one(0, decltype(n)::value); });
+  wait_vmcnt<0>();
+  lds_barrier();
+  half8 b0[kWSub], b1[kWSub], a_h[2];
+#pragma unroll
+  for (int j = 0; j < kWSub; ++j) b0[j] = rd(0, 1, j);
+  a_h[0] = rd(0, 0, 0);
+  auto step = [&](int kt, half8 (&bc)[kWSub], half8 (&bn)[kWSub]) {
+    static_for<kWSub>([&](auto I) {
+      constexpr int i = decltype(I)::value, c = i & 1;
+      if constexpr (i == kWSub - 1) {
+        wait_vmcnt<0>();
+        lds_barrier();
+        a_h[c ^ 1] = rd(kt + 1, 0, 0);
+#pragma unroll
+        for (int j = 0; j < kWSub; ++j) bn[j] = rd(kt + 1, 1, j);
+      } else {
+        a_h[c ^ 1] = rd(kt, 0, i + 1);
+        if constexpr (i < 4) {
+          dma_one(kt + 1, 2 * i);
+          dma_one(kt + 1, 2 * i + 1);
+        }
+      }
+      SCHED_FENCE();
+      static_for<kWSub>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        mfma16_acc(acc[i][j], a_h[c], bc[j]);
+      });
+      SCHED_FENCE();
+    });
+  };
+  for (int kt = 0; kt < ksteps; kt += 2) {
+    step(kt, b0, b1);
+    step(kt + 1, b1, b0);
+  }
+  wait_vmcnt<0>();
+  mfma_drain();
+
+  const int col0 = tn * kWide + wn * 128 + (lane & 15);
+  const int row0 = tm * kWide + wm * 128 + (lane >> 4) * 4;
+  const bool full = (tm + 1) * kWide <= M && (tn + 1) * kWide <= N;
+  store_tile16<kWSub, kWSub>(C, ldc, M, N, row0, col0, full,
+                             [&](int i, int j, int r) { return acc[i][j][r]; });
+}
+
 // ---------------------------------------------------------------------------
 // 256 x 128 tiles: termwise and the unscaled elementwise fallback.
 constexpr int kNarrowM = 256;
@@ -490,19 +550,31 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
 }
 
 
-template <int V, int S = kWideStages>
-hipError_t launch_wide(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                       hipStream_t stream) {
-  constexpr size_t lds = wide_lds_bytes<V, S>();
+template <bool kPrefetch>
+hipError_t launch_el(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
+                     hipStream_t stream) {
   static std::atomic<bool> done[kMaxDevices];
-  const hipError_t attr = set_lds(&gemm_wide_kernel<V, S>, lds, done);
+  const hipError_t attr = set_lds(&gemm_el_kernel<kPrefetch>, kElLdsBytes, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kWide);
   const int tiles_n = static_cast<int>(p.Np / kWide);
-  hipLaunchKernelGGL((gemm_wide_kernel<V, S>), dim3(tiles_m * tiles_n), dim3(kWideThreads), lds,
-                     stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
+  hipLaunchKernelGGL((gemm_el_kernel<kPrefetch>), dim3(tiles_m * tiles_n), dim3(kWideThreads),
+                     kElLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
                      static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
                      static_cast<int>(N), s, 1.0f / s);
+  return hipGetLastError();
+}
+
+hipError_t launch_hi(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                     hipStream_t stream) {
+  static std::atomic<bool> done[kMaxDevices];
+  const hipError_t attr = set_lds(&gemm_hi_kernel, kHiLdsBytes, done);
+  if (attr != hipSuccess) return attr;
+  const int tiles_m = static_cast<int>(p.Mp / kWide);
+  const int tiles_n = static_cast<int>(p.Np / kWide);
+  hipLaunchKernelGGL(gemm_hi_kernel, dim3(tiles_m * tiles_n), dim3(kWideThreads), kHiLdsBytes,
+                     stream, p.a_hi, p.b_hi, static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc,
+                     static_cast<int>(M), static_cast<int>(N));
   return hipGetLastError();
 }
 
@@ -531,13 +603,13 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
                        float scale, int variant, int cus, hipStream_t stream) {
   switch (variant) {
     case kElementwise: {
-      const hipError_t e = launch_wide<kElementwise>(p, M, N, C, ldc, scale, stream);
+      const hipError_t e = launch_el<true>(p, M, N, C, ldc, scale, stream);
       if (e != hipSuccess) return e;
       return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
     }
     case kTermwise: return launch_narrow<kTermwise>(p, M, N, C, ldc, scale, cus, stream);
     case kCrossFirst: return launch_narrow<kCrossFirst>(p, M, N, C, ldc, scale, cus, stream);
-    case kHiOnly: return launch_wide<kHiOnly>(p, M, N, C, ldc, scale, stream);
+    case kHiOnly: return launch_hi(p, M, N, C, ldc, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -551,8 +623,8 @@ hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, i
                               float scale, int stages, int cus, hipStream_t stream) {
   hipError_t e = hipSuccess;
   switch (stages) {
-    case 1: e = launch_wide<kElementwise, 1>(p, M, N, C, ldc, scale, stream); break;
-    case 2: e = launch_wide<kElementwise, 2>(p, M, N, C, ldc, scale, stream); break;
+    case 1: e = launch_el<false>(p, M, N, C, ldc, scale, stream); break;
+    case 2: e = launch_el<true>(p, M, N, C, ldc, scale, stream); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

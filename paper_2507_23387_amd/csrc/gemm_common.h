@@ -4,6 +4,7 @@
 #pragma once
 
 #include <atomic>
+#include <utility>
 
 #include "internal.h"
 
@@ -28,6 +29,20 @@ __device__ __forceinline__ floatx16 mfma32(const half8& a, const half8& b, const
 // with wait_vmcnt<>() before the barrier that publishes a stage.
 __device__ __forceinline__ void dma16(const void* g, unsigned lds_addr) {
   asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_addr) : "memory");
+}
+
+// The same DMA with the global base in an SGPR pair and a per-lane 32-bit
+// byte offset (the saddr form): the wave-uniform part of the address costs
+// scalar instructions only.  `base` must be wave-uniform; readfirstlane makes
+// the compiler keep it in SGPRs.
+__device__ __forceinline__ void dma16s(const void* base, unsigned voff, unsigned lds_addr) {
+  // readfirstlane returns a signed int: take both words as uint32_t before
+  // widening, so the low word is zero-extended.
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)));
+  const uint64_t sb = (static_cast<uint64_t>(hi) << 32) | lo;
+  asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sb), "{m0}"(lds_addr) : "memory");
 }
 
 template <int N>
@@ -131,6 +146,49 @@ __device__ __forceinline__ void store_tile(float* __restrict__ C, int64_t ldc, i
 // step; D element (row 4*(l/16) + r, column l%16) is in register r.
 __device__ __forceinline__ floatx4 mfma16(const half8& a, const half8& b, const floatx4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// acc += A B on v_mfma_f32_16x16x32_f16 (operands as for mfma16), with the
+// accumulator tied to one AGPR quad ("+a") so that the register allocator
+// keeps every accumulator in place across the main loop.  The compiler does
+// not see an MFMA here, so the callers keep the MFMA hazards themselves:
+// dependent MFMAs on one accumulator are at least 8 MFMAs apart, operand
+// registers are written at least 8 MFMAs before or after they are read, and
+// the accumulators are read by other instructions only after
+// mfma_drain().
+__device__ __forceinline__ void mfma16_acc(floatx4& acc, const half8& a, const half8& b) {
+  asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+// x * s for the eight halves of x, s given as a packed pair (s, s): four
+// v_pk_mul_f16 issued as volatile asm, so that the compiler neither moves nor
+// rematerializes them next to an mfma16_acc that reads the result (it would
+// not see that hazard); the callers place them at least 8 MFMAs ahead.
+__device__ __forceinline__ half8 pk_scale(const half8& x, uint32_t s2) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_bit_cast(u32x4, x);
+  uint32_t r0, r1, r2, r3;
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r0) : "s"(s2), "v"(v.x));
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r1) : "s"(s2), "v"(v.y));
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r2) : "s"(s2), "v"(v.z));
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r3) : "s"(s2), "v"(v.w));
+  return __builtin_bit_cast(half8, u32x4{r0, r1, r2, r3});
+}
+
+// Wait states after the last mfma16_acc before its accumulators are read.
+__device__ __forceinline__ void mfma_drain() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>{}) for I = 0 .. N-1, so
+// every index in the body is a constant expression (no reliance on unrolling).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 // Store a wave's 16 x 16 accumulators: register r of MFMA tile (i, j) holds
