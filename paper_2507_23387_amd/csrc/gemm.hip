@@ -115,8 +115,8 @@ __device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off
 //   - reads the A fragments of step kt+1 into a second register set, two or
 //     three per column block (blocks 0-6), the two sets swapping roles each
 //     step;
-//   - copies B stage kt+1 and A stage kt+2 into LDS with 16 DMAs issued in
-//     column blocks 0 and 1, so each has most of the step to land;
+//   - copies B stage kt+1 and A stage kt+2 into LDS with 16 DMAs, four in
+//     each of column blocks 0-3 (bursts of DMAs stall the wave's issue);
 // and every LDS read, DMA and VALU instruction sits between two MFMAs.  One
 // barrier per step, before the last column block, publishes B stage kt+1 and
 // A stage kt+2 and retires the slots of B stage kt and A stage kt+1.  Stages
@@ -130,8 +130,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
   constexpr int kBBase = 2 * kSlotHalves;     // the B slots follow the two A slots
-  constexpr int kDmaCols = 2;                 // column blocks that issue the DMAs
-  constexpr int kDmaPerCol = 16 / kDmaCols;   // after MFMAs 2, 5, ..., 23 of a block
+  constexpr int kDmaCols = 4;                 // column blocks that issue the DMAs
+  constexpr int kDmaPerCol = 16 / kDmaCols;   // after MFMAs 2, 8, 14, 20 of a block
   if (range[0] == range[1]) return;  // s B_hi overflows FP16: the narrow kernel runs instead
   extern __shared__ __align__(16) uint16_t lds[];
 
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
   // One step.  Column block j issues HH(., j), XA(., j), XB(., j), so every
   // accumulator sees the block terms in the order HH, XA, XB, and the three
   // MFMAs of one accumulator are 8 MFMAs apart.  After MFMA m of a block:
-  // m = 1, 9, 17 read the next A fragments, m = 2, 5, ..., 23 of blocks 0-1
+  // m = 1, 9, 17 read the next A fragments, m = 2, 8, 14, 20 of blocks 0-3
   // issue the DMAs, m = 14 forms the next block's s B_hi.
   auto step = [&](int kt, half8 (&ah)[kWSub], half8 (&al)[kWSub], half8 (&nh)[kWSub],
                   half8 (&nl)[kWSub]) {
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
               nl[r - kWSub] = rd_a(kt + 1, 1, r - kWSub);
           }
         }
-        if constexpr (kPrefetch && j < kDmaCols && m % 3 == 2) dma(kt, j * kDmaPerCol + m / 3);
+        if constexpr (kPrefetch && j < kDmaCols && m % 6 == 2) dma(kt, j * kDmaPerCol + m / 6);
         SCHED_FENCE();
       });
     });
