@@ -365,6 +365,172 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Termwise kernel (Eq. termwise) on v_mfma_f32_16x16x32_f16: one 256 x 128
+// tile of C per workgroup, 4 waves of 64 x 128 (one per SIMD).  Three FP32
+// accumulators run over all of K, HH = A_hi B_hi, XA = A_lo B_hi and
+// XB = A_hi B_lo, and the epilogue forms C = (HH + XA / s) + XB / s.  The
+// 3 x 128 accumulator registers of a wave are HH and XA in the 256 AGPRs and
+// XB in VGPRs, every one tied to its registers through mfma16_acc.
+//
+// The data path is the elementwise kernel's at half the width: LDS holds two
+// A slots (A_hi, A_lo of 256 rows x 32 k: 32 KiB) and two B slots (B_hi,
+// B_lo of 128 columns: 16 KiB).  A wave keeps its 64 rows of A for the step
+// in registers and streams B one 16-column block at a time, one block ahead;
+// during step kt it reads the A fragments of step kt+1 into a second set (one
+// or two per block, blocks 0-6) and issues 12 DMAs (B stage kt+1, A stage
+// kt+2; two in each of blocks 0-5).  One barrier per step, before the last
+// block, publishes B stage kt+1 and A stage kt+2 and retires B stage kt and
+// A stage kt+1.  Each accumulator is updated once per step (MFMAs on one
+// accumulator are 96 apart).
+constexpr int kTwM = 256;
+constexpr int kTwN = 128;
+constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
+constexpr int kTwBSlot = 2 * kTwN * kStep;        // halves: B_hi, B_lo of one step
+constexpr size_t kTwLdsBytes = static_cast<size_t>(2) * (kTwASlot + kTwBSlot) * 2;  // 96 KiB
+
+__global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
+    const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
+    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo, int Kp, int tiles_m,
+    int tiles_n, float* __restrict__ C, int64_t ldc, int M, int N, float inv_s) {
+  constexpr int kRows = 4;                   // 16-row blocks per wave
+  constexpr int kCols = 8;                   // 16-column blocks per wave
+  constexpr int kAPlane = kTwM * kStep;      // one A plane of one step: 8 tiles... 16 KiB
+  constexpr int kBPlane = kTwN * kStep;      // one B plane of one step: 8 KiB
+  constexpr int kBBase = 2 * kTwASlot;       // the B slots follow the two A slots
+  extern __shared__ __align__(16) uint16_t lds[];
+
+  int tm, tn;
+  if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn))
+    tile_of<4>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t slices = Kp / kSlice;
+  const int ksteps = static_cast<int>(slices / 2);
+
+  // A stage: tiles (panel ph, slice sl) of the tile's two A panels at
+  // position 2*ph + sl of each plane; B stage: tiles (slice sl) of its one B
+  // panel at position sl.  Wave w copies 1 KiB block w of every tile.
+  const int64_t panel_stride = slices * kTileHalves;
+  const unsigned lane_off = static_cast<unsigned>(w * 512 + lane * 8) * 2;  // bytes
+  const uint16_t* const src_a[2] = {a_hi + 2 * tm * panel_stride, a_lo + 2 * tm * panel_stride};
+  const uint16_t* const src_b[2] = {b_hi + tn * panel_stride, b_lo + tn * panel_stride};
+  const unsigned lds_base = lds_address(lds) + w * 1024;
+  auto dma_a = [&](int t, int n) {  // n < 8
+    const int tc = min(t, ksteps - 1);
+    const int p = n >> 2, ph = (n >> 1) & 1, sl = n & 1;
+    dma16s(src_a[p] + ph * panel_stride + static_cast<int64_t>(2 * tc + sl) * kTileHalves,
+           lane_off,
+           lds_base + ((t & 1) * kTwASlot + p * kAPlane + (2 * ph + sl) * kTileHalves) * 2);
+  };
+  auto dma_b = [&](int t, int n) {  // n < 4
+    const int tc = min(t, ksteps - 1);
+    const int p = n >> 1, sl = n & 1;
+    dma16s(src_b[p] + static_cast<int64_t>(2 * tc + sl) * kTileHalves, lane_off,
+           lds_base + (kBBase + (t & 1) * kTwBSlot + p * kBPlane + sl * kTileHalves) * 2);
+  };
+  // The d-th of the 12 DMAs of step kt: B stage kt+1, then A stage kt+2.
+  auto dma = [&](int kt, int d) {
+    if (d < 4)
+      dma_b(kt + 1, d);
+    else
+      dma_a(kt + 2, d - 4);
+  };
+
+  // Wave w's rows are rows 64 (w & 1) .. 64 (w & 1) + 63 of A panel w >> 1;
+  // block i (16 rows) of them and column block j of the B panel are read as
+  // in the elementwise kernel (row bit 4 = parity of the block).
+  int a_off[2], b_off[2];
+  wide_frag_offsets(lane, w >> 1, a_off);
+  wide_frag_offsets(lane, 0, b_off);
+  const int a_row = 64 * (w & 1) * kSlice;
+  auto rd_a = [&](int t, int p, int i) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + (t & 1) * kTwASlot + p * kAPlane + a_off[i & 1] +
+                                           a_row + i * 16 * kSlice);
+  };
+  auto rd_b = [&](int t, int p, int j) -> half8 {
+    return *reinterpret_cast<const half8*>(lds + kBBase + (t & 1) * kTwBSlot + p * kBPlane +
+                                           b_off[j & 1] + j * 16 * kSlice);
+  };
+
+  floatx4 hh[kRows][kCols], xa[kRows][kCols], xb[kRows][kCols];
+#pragma unroll
+  for (int i = 0; i < kRows; ++i)
+#pragma unroll
+    for (int j = 0; j < kCols; ++j) hh[i][j] = xa[i][j] = xb[i][j] = floatx4{};
+
+  static_for<8>([&](auto n) { dma_a(0, decltype(n)::value); });
+  static_for<8>([&](auto n) { dma_a(1, decltype(n)::value); });
+  static_for<4>([&](auto n) { dma_b(0, decltype(n)::value); });
+  wait_vmcnt<0>();
+  lds_barrier();
+  half8 AH[kRows], AL[kRows], NH[kRows], NL[kRows], bh[2], bl[2];
+#pragma unroll
+  for (int i = 0; i < kRows; ++i) {
+    AH[i] = rd_a(0, 0, i);
+    AL[i] = rd_a(0, 1, i);
+  }
+  bh[0] = rd_b(0, 0, 0);
+  bl[0] = rd_b(0, 1, 0);
+  lds_barrier();  // A slot 0 is refilled (stage 2) during step 0
+
+  // Column block j issues HH(., j), XA(., j), XB(., j).  After MFMA m of a
+  // block: m = 1, 7 read the next A fragments, m = 3, 9 of blocks 0-5 issue
+  // the DMAs.
+  auto step = [&](int kt, half8 (&ah)[kRows], half8 (&al)[kRows], half8 (&nh)[kRows],
+                  half8 (&nl)[kRows]) {
+    static_for<kCols>([&](auto J) {
+      constexpr int j = decltype(J)::value, c = j & 1;
+      if constexpr (j == kCols - 1) {
+        wait_vmcnt<0>();
+        lds_barrier();
+        bh[c ^ 1] = rd_b(kt + 1, 0, 0);
+        bl[c ^ 1] = rd_b(kt + 1, 1, 0);
+      } else {
+        bh[c ^ 1] = rd_b(kt, 0, j + 1);
+        bl[c ^ 1] = rd_b(kt, 1, j + 1);
+      }
+      SCHED_FENCE();
+      // A fragments rb .. re-1 of the 8 (A_hi blocks 0-3, then A_lo).
+      constexpr int rb = (8 * j + 6) / 7, re = (8 * (j + 1) + 6) / 7;
+      static_for<3 * kRows>([&](auto Mc) {
+        constexpr int m = decltype(Mc)::value, g = m / kRows, i = m % kRows;
+        if constexpr (g == 0)
+          mfma16_acc(hh[i][j], ah[i], bh[c]);
+        else if constexpr (g == 1)
+          mfma16_acc(xa[i][j], al[i], bh[c]);
+        else
+          mfma16_vacc(xb[i][j], ah[i], bl[c]);
+        SCHED_FENCE();
+        if constexpr (j < kCols - 1 && (m == 1 || m == 7)) {
+          constexpr int r = rb + m / 6;
+          if constexpr (r < re) {
+            if constexpr (r < kRows)
+              nh[r] = rd_a(kt + 1, 0, r);
+            else
+              nl[r - kRows] = rd_a(kt + 1, 1, r - kRows);
+          }
+        }
+        if constexpr (j < 6 && (m == 3 || m == 9)) dma(kt, 2 * j + m / 6);
+        SCHED_FENCE();
+      });
+    });
+  };
+  for (int kt = 0; kt < ksteps; kt += 2) {
+    step(kt, AH, AL, NH, NL);
+    step(kt + 1, NH, NL, AH, AL);
+  }
+  wait_vmcnt<0>();
+  mfma_drain();
+
+  const int col0 = tn * kTwN + (lane & 15);
+  const int row0 = tm * kTwM + w * 64 + (lane >> 4) * 4;
+  const bool full = (tm + 1) * kTwM <= M && (tn + 1) * kTwN <= N;
+  store_tile16<kRows, kCols>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
+    return __builtin_fmaf(xb[i][j][r], inv_s, __builtin_fmaf(xa[i][j][r], inv_s, hh[i][j][r]));
+  });
+}
+
+// ---------------------------------------------------------------------------
 // 256 x 128 tiles: termwise and the unscaled elementwise fallback.
 constexpr int kNarrowM = 256;
 constexpr int kNarrowN = 128;
@@ -578,6 +744,19 @@ hipError_t launch_hi(const Planes& p, int64_t M, int64_t N, float* C, int64_t ld
   return hipGetLastError();
 }
 
+hipError_t launch_tw(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
+                     hipStream_t stream) {
+  static std::atomic<bool> done[kMaxDevices];
+  const hipError_t attr = set_lds(&gemm_tw_kernel, kTwLdsBytes, done);
+  if (attr != hipSuccess) return attr;
+  const int tiles_m = static_cast<int>(p.Mp / kTwM);
+  const int tiles_n = static_cast<int>(p.Np / kTwN);
+  hipLaunchKernelGGL(gemm_tw_kernel, dim3(tiles_m * tiles_n), dim3(kWideThreads), kTwLdsBytes,
+                     stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, static_cast<int>(p.Kp), tiles_m,
+                     tiles_n, C, ldc, static_cast<int>(M), static_cast<int>(N), 1.0f / s);
+  return hipGetLastError();
+}
+
 template <int V>
 hipError_t launch_narrow(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
                          int cus, hipStream_t stream) {
@@ -607,7 +786,7 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
       if (e != hipSuccess) return e;
       return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
     }
-    case kTermwise: return launch_narrow<kTermwise>(p, M, N, C, ldc, scale, cus, stream);
+    case kTermwise: return launch_tw(p, M, N, C, ldc, scale, stream);
     case kCrossFirst: return launch_narrow<kCrossFirst>(p, M, N, C, ldc, scale, cus, stream);
     case kHiOnly: return launch_hi(p, M, N, C, ldc, stream);
     default: return hipErrorInvalidValue;

@@ -175,6 +175,11 @@ __device__ __forceinline__ half8 pk_scale(const half8& x, uint32_t s2) {
   return __builtin_bit_cast(half8, u32x4{r0, r1, r2, r3});
 }
 
+// The same with the accumulator tied to a VGPR quad.
+__device__ __forceinline__ void mfma16_vacc(floatx4& acc, const half8& a, const half8& b) {
+  asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+}
+
 // Wait states after the last mfma16_acc before its accumulators are read.
 __device__ __forceinline__ void mfma_drain() {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
