@@ -2,54 +2,30 @@
 //
 // For each tile of C it forms (Eq. recover_eqn of arXiv 2507.23387)
 //   HH = A_hi B_hi,  XA = A_lo B_hi,  XB = A_hi B_lo
-// with v_mfma_f32_32x32x16_f16 (FP16 x FP16 products are exact; the MFMA adds
-// the 16 products of a k-step to its C operand in one fused, once-rounded FP32
-// operation) and reconstructs C in the accumulation order asked for.
+// (FP16 x FP16 products are exact; an MFMA adds the products of a k-step to
+// its C operand in one fused, once-rounded FP32 operation) and reconstructs
+// C in the accumulation order asked for.
 //
-// Two kernels share one data path:
-//
-// gemm_wide_kernel, 256 x 256 tiles, 4 waves of 128 x 128 (one per SIMD, the
-// 256-register accumulator in AGPRs):
-//   kElementwise (Eq. elementwise, Sec. 4.5) with the contraction cut into
-//     blocks g of one k-step (16).  The accumulator holds s * acc, so that the
-//     three per-block additions of the equation become three chained MFMAs:
-//       s*acc <- fl(s*acc + A_hi (s B_hi))   = s * fl(acc + HH_g)
-//       s*acc <- fl(s*acc + A_lo B_hi)       = s * fl(acc + XA_g / s)
-//       s*acc <- fl(s*acc + A_hi B_lo)       = s * fl(acc + XB_g / s)
-//     and C = (s*acc) / s at the end.  s B_hi is formed in registers with
-//     v_pk_mul_f16; it is exact because s is a power of two, provided
-//     |B_hi| s <= 65504, which the split of B checks (the range flag).  Each
-//     block term is summed by the MFMA together with the accumulator, with
-//     one rounding, instead of being rounded to FP32 on its own first.
-//   kHiOnly: C = HH, the native-FP16 GEMM baseline.
-//
-// gemm_narrow_kernel, 256 x 128 tiles, 8 waves of 64 x 64 (two per SIMD):
-//   kTermwise (Eq. termwise): three FP32 accumulators over all of K,
-//     C = (HH + XA / s) + XB / s in the epilogue.
-//   kCrossFirst (the reordered elementwise accumulation proposed at the end
-//     of Sec. 4.5): per block g of two k-steps the cross products are summed
-//     first, X_g = XA_g + XB_g (one MFMA chain), HH_g separately, and
-//     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
-//   kElementwise when the range flag is set: unscaled, blocks of two k-steps
-//     (32): HH goes straight into the accumulator, XA_g and XB_g into block
-//     sums started from zero, and acc = (acc + XA_g / s) + XB_g / s with two
-//     v_fma_f32 at the end of each block (1/s is exact).
+// Kernels:
+//   gemm_el_kernel   256 x 256 tiles, v_mfma_f32_16x16x32_f16: the scaled
+//                    elementwise order (Eq. elementwise, Sec. 4.5), one
+//                    accumulator holding s * acc, blocks of one 32-wide
+//                    k-step.
+//   gemm_tw_kernel   256 x 128 tiles, v_mfma_f32_16x16x32_f16: the termwise
+//                    order (Eq. termwise), three accumulators.
+//   gemm_hi_kernel   256 x 256 tiles: HH only, the native-FP16 baseline.
+//   gemm_narrow_kernel  256 x 128 tiles, v_mfma_f32_32x32x16_f16: the
+//                    unscaled elementwise fallback (range flag set) and the
+//                    cross-terms-first order (end of Sec. 4.5).
 // Both elementwise kernels are launched; each reads the range flag first and
 // the one that does not apply returns at once.
 //
 // Data path.  The planes are stored as 4 KiB tiles of 128 rows x 16 k in the
 // order and swizzle the LDS wants (internal.h), so one pipeline stage (one
-// k-step of every plane the kernel needs) is a few contiguous 4 KiB blocks,
-// copied from global memory straight into LDS with global_load_lds_dwordx4 (no
-// VGPR staging).  Stages go into a ring of kStages slots.  In k-step kt the
-// fragments of step kt+1 are read while the MFMAs of step kt run: each
-// fragment register is reloaded as soon as its last MFMA of the step has been
-// issued (a rolling schedule; it fits the register file where double
-// buffering does not), and the DMAs for stage kt+kStages are spread between
-// the MFMA groups so the in-order wave never stalls on a burst of memory
-// instructions.  One s_barrier per step both publishes stage kt+1 and retires
-// the slot of stage kt before it is refilled.  Past the last stage the loads
-// repeat the last stage, so every wait count is a compile-time constant.
+// k-step of a plane) is a few contiguous 4 KiB blocks, copied from global
+// memory straight into LDS with global_load_lds_dwordx4 (no VGPR staging).
+// Every wait count is a compile-time constant: past the last stage the loads
+// repeat the last stage.  Each kernel's comment describes its schedule.
 #include <algorithm>
 #include <atomic>
 
@@ -531,7 +507,23 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// 256 x 128 tiles: termwise and the unscaled elementwise fallback.
+// 256 x 128 tiles on v_mfma_f32_32x32x16_f16, 8 waves of 64 x 64 (two per
+// SIMD), three 64-register accumulator sets in VGPRs:
+//   kElementwise when the range flag is set: unscaled, blocks of two k-steps
+//     (32): HH goes straight into the accumulator, XA_g and XB_g into block
+//     sums started from zero, and acc = (acc + XA_g / s) + XB_g / s with two
+//     v_fma_f32 at the end of each block (1/s is exact).
+//   kCrossFirst (the reordered elementwise accumulation proposed at the end
+//     of Sec. 4.5): per block g of two k-steps the cross products are summed
+//     first, X_g = XA_g + XB_g (one MFMA chain), HH_g separately, and
+//     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
+// Stages of one 16-k slice of the four planes go into a 4-slot LDS ring.  In
+// k-step kt the fragments of step kt+1 are read while the MFMAs of step kt
+// run: each fragment register is reloaded as soon as its last MFMA of the
+// step has been issued, and the DMAs for stage kt+4 are spread between the
+// MFMA groups.  One s_barrier per step publishes stage kt+1 and retires the
+// slot of stage kt.  A persistent grid of one workgroup per compute unit
+// walks the tiles.
 constexpr int kNarrowM = 256;
 constexpr int kNarrowN = 128;
 constexpr int kNarrowThreads = 512;
@@ -545,7 +537,7 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
-  static_assert(V == kElementwise || V == kTermwise || V == kCrossFirst, "narrow kernel variants");
+  static_assert(V == kElementwise || V == kCrossFirst, "narrow kernel variants");
   constexpr int S = kNarrowStages;
   constexpr int kAHalves = kNarrowM * kSlice;  // A plane slot: two tiles
   constexpr int kBHalves = kNarrowN * kSlice;  // B plane slot: one tile
@@ -620,10 +612,9 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
     // One k-step: XA, then HH, then XB; each fragment is reloaded with step
     // kt+1 once its last MFMA of the step is issued.  `first` marks the first
     // step of a block (block sums restart), `last` its end (fold).  Register
-    // sets: termwise acc = HH, xa = XA, xb = XB; elementwise fallback acc =
-    // running sum, xa = XA_g, xb = XB_g; cross-first acc = running sum, xa =
-    // X_g = XA_g + XB_g, xb = HH_g.
-    constexpr bool kBlocks = V != kTermwise;
+    // sets: elementwise fallback acc = running sum, xa = XA_g, xb = XB_g;
+    // cross-first acc = running sum, xa = X_g = XA_g + XB_g, xb = HH_g.
+    constexpr bool kBlocks = true;
     auto step = [&](int kt, bool first, bool last) {
       const int nk = kt + 1;
 #pragma unroll
@@ -704,14 +695,8 @@ __global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
     const int col0 = tn * kNarrowN + wn * 64 + (lane & 31);
     const int row0 = tm * kNarrowM + wm * 64 + (lane >> 5) * 4;
     const bool full = (tm + 1) * kNarrowM <= M && (tn + 1) * kNarrowN <= N;
-    store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
-      float v = acc[i][j][r];
-      if constexpr (V == kTermwise) {
-        v = __builtin_fmaf(xa[i][j][r], inv_s, v);
-        v = __builtin_fmaf(xb[i][j][r], inv_s, v);
-      }
-      return v;
-    });
+    store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full,
+                           [&](int i, int j, int r) { return acc[i][j][r]; });
   }
 }
 
