@@ -346,3 +346,38 @@ def test_workload_parity_sampled_rows(gpu, name, order, scale):
         coef = float(bounds.main_bound_coef(w.K))
         err = np.abs(C[rows].astype(np.float64) - ref64(A, B, rows))
         assert np.all(err <= coef * absab)
+
+
+def test_workspace_at_high_addresses(gpu):
+    """A caller workspace placed so that the FP16 planes sit at addresses whose
+    low 32 bits are >= 2^31 and one plane straddles a 4 GiB boundary: the GEMM
+    kernels build each copy's 64-bit source address from two 32-bit halves,
+    and every order must give the same bits as with a pool workspace."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    M, N, K = 520, 300, 1056
+    A, B = workloads.make_operands(M, N, K, 14, "uniform_pm1")
+    dA, dB = to_dev(A), to_dev(B)
+    stream = torch.cuda.current_stream().cuda_stream
+    wsb = max(binding.sgemm_cube_workspace_size(M, N, K, binding.ORDERS[o]) for o in ORDERS)
+    plane = binding.sgemm_cube_workspace_size(M, N, K) // 4
+    buf = torch.empty((1 << 32) + wsb + 4096, dtype=torch.uint8, device="cuda")
+    base = buf.data_ptr()
+    # The workspace starts 1.5 planes below a 4 GiB boundary (256-byte aligned).
+    target = ((1 << 32) - (3 * plane) // 2) & ~255
+    off = (target - (base & 0xFFFFFFFF)) % (1 << 32)
+    ws_ptr = base + off
+    assert off + wsb <= buf.numel() and ws_ptr % 256 == 0
+    assert ws_ptr & 0xFFFFFFFF >= 1 << 31
+    assert (ws_ptr >> 32) != ((ws_ptr + wsb - 1) >> 32)
+    for order in ORDERS:
+        log(f"high-address workspace {order}")
+        ref = binding.matmul(dA, dB, 2048.0, order)
+        C = torch.empty_like(ref)
+        assert binding.sgemm_cube_ws(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, C.data_ptr(),
+                                     N, 2048.0, binding.ORDERS[order], ws_ptr, wsb, stream) == 0
+        torch.cuda.synchronize()
+        assert torch.equal(C, ref), order
+    del buf
