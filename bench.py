@@ -72,6 +72,17 @@ def traffic_entry(workload: str, order: str):
     return data.get("entries", {}).get(f"{workload}/{order}")
 
 
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(A, B, w, scale, order, target_s: float):
     """Time the oracle (as it stands) on a bounded sample of output rows.
 
@@ -103,6 +114,7 @@ def cpu_baseline(A, B, w, scale, order, target_s: float):
         "value": flops / t / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
+        "cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": f"{len(rows)} of {w.M} output rows of {w.name} ({order}, s=2^"
                   f"{int(np.log2(scale))}), full K={w.K} and N={w.N}; the oracle's split of "
@@ -236,6 +248,7 @@ def main():
     total_ms = ev[0][0].elapsed_time(ev[-1][2])
     split_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    step_times = np.array([e[0].elapsed_time(e[2]) for e in ev])
     ms_per_step = total_ms / args.steps
     flops = 2.0 * M * N * K
     value = flops / (ms_per_step * 1e-3) / 1e12
@@ -246,6 +259,9 @@ def main():
     # A plain device copy of known size, outside the timed region: the
     # rocprofv3 FETCH_SIZE / WRITE_SIZE counters of this dispatch calibrate
     # the same counters read for the GEMM kernel.
+    # Its bandwidth (bytes read + written) is also the practical ceiling the
+    # HBM-bound split is compared with.
+    copy_gbs = None
     if args.copy_mib > 0:
         n = args.copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -253,6 +269,14 @@ def main():
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        for _ in range(5):
+            dst.copy_(src)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        copy_gbs = 2 * 4 * n * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
         del src, dst
 
     gemm_tflops = 3 * flops / (gemm_ms * 1e-3) / 1e12
@@ -276,7 +300,10 @@ def main():
         "three_gemm_peak_tflops": THREE_GEMM_PEAK_TFLOPS,
         "split_ms": split_ms,
         "split_gbs": split_bytes / (split_ms * 1e-3) / 1e9,
+        "device_copy_gbs": copy_gbs,
         "gemm_ms": gemm_ms,
+        "step_ms": {"median": float(np.median(step_times)), "min": float(step_times.min()),
+                    "max": float(step_times.max())},
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
 

@@ -13,6 +13,10 @@
     python bench_profile.py busy DIR
         MFMA busy fraction and average shader clock per GEMM dispatch from a
         `--pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CYCLES` pass
+    python bench_profile.py lds_l2 DIR
+        LDS bank conflicts and L2 hit rate per GEMM dispatch from a
+        `--pmc SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_INSTS_LDS TCC_HIT_sum
+        TCC_MISS_sum` pass
 
 Reads only the CSV files rocprofv3 wrote; runs nothing on the GPU.
 """
@@ -167,6 +171,28 @@ def busy(directory: str) -> str:
     return "\n".join(lines)
 
 
+def lds_l2(directory: str) -> str:
+    """LDS bank conflicts and L2 hit rate per GEMM dispatch from a
+    `--pmc SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_INSTS_LDS TCC_HIT_sum
+    TCC_MISS_sum` pass."""
+    conf = counters(directory, "SQ_LDS_BANK_CONFLICT")
+    active = counters(directory, "SQ_LDS_IDX_ACTIVE")
+    insts = counters(directory, "SQ_INSTS_LDS")
+    hit = counters(directory, "TCC_HIT_sum")
+    miss = counters(directory, "TCC_MISS_sum")
+    lines = ["| kernel | LDS instructions | LDS bank-conflict cycles | conflict / LDS active | "
+             "L2 hits | L2 misses | L2 hit rate |", "|---|---|---|---|---|---|---|"]
+    for k in sorted(conf):
+        if "gemm" not in k or k not in hit:
+            continue
+        for c, a, n, h, m in zip(conf[k], active[k], insts[k], hit[k], miss[k]):
+            if n < 1e6:
+                continue
+            lines.append(f"| {short(k)} | {n:.4g} | {c:.4g} | {100 * c / max(a, 1):.2f}% | "
+                         f"{h:.4g} | {m:.4g} | {100 * h / max(h + m, 1):.1f}% |")
+    return "\n".join(lines)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -180,14 +206,18 @@ def main():
     b.add_argument("--copy-mib", type=int, default=512)
     c = sub.add_parser("busy")
     c.add_argument("dir")
+    d = sub.add_parser("lds_l2")
+    d.add_argument("dir")
     args = ap.parse_args()
     if args.cmd == "stats":
         print(stats(args.dir))
     elif args.cmd == "traffic":
         print(traffic(args.fetch_dir, args.write_dir, workloads.get(args.workload).name,
                       args.order, args.copy_mib))
-    else:
+    elif args.cmd == "busy":
         print(busy(args.dir))
+    else:
+        print(lds_l2(args.dir))
 
 
 if __name__ == "__main__":
