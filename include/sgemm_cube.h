@@ -199,12 +199,12 @@ int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_
 /*
  * Measurement hook for the pipeline ablation (Sec. 5.4 measures double
  * buffering against a single buffer): sgemm_cube_compute with the elementwise
- * order, running the 256 x 256 kernel with `stages` LDS stage slots of one
- * 32-wide k-step each (64 KiB), 1 <= stages <= 2.  stages = 1 copies each
- * k-step's operands into LDS and waits for them inside the step (no
- * prefetch); stages = 2 (the library's own choice) keeps the copy of the next
- * step in flight while a step computes.  Results are identical for both stage
- * counts.  accum_order other than SGEMM_CUBE_ELEMENTWISE ->
+ * order on the 256 x 256 kernel, 1 <= stages <= 2.  stages = 2 (the library's
+ * own choice) copies the operands of the coming k-steps into LDS while a step
+ * computes; stages = 1 issues the same copies at the end of each step and
+ * waits for them there, so no copy overlaps the matrix instructions.  Both
+ * use the same LDS slots and compute identical results.
+ * accum_order other than SGEMM_CUBE_ELEMENTWISE ->
  * SGEMM_CUBE_ERR_NOT_SUPPORTED; stages outside 1..2 ->
  * SGEMM_CUBE_ERR_INVALID_VALUE; otherwise as sgemm_cube_compute
  * (when the range flag selects the unscaled fallback kernel, that kernel

@@ -146,9 +146,10 @@ hipError_t launch_range_report(const Planes& p, bool empty, uint32_t* out, hipSt
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                        float scale, int variant, int cus, hipStream_t stream);
 
-// The elementwise GEMM with an explicit number of LDS stage slots of the
-// 256 x 256 kernel (1 or 2; the library's default is 2), for the pipeline
-// ablation.  The fallback kernel (range flag set) keeps its own depth.
+// The elementwise GEMM with the copies of the 256 x 256 kernel overlapped
+// with its MFMAs (stages = 2, the library's default) or issued and waited for
+// at the end of each step (stages = 1), for the pipeline ablation.  The
+// fallback kernel (range flag set) keeps its own pipeline.
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, int cus, hipStream_t stream);
 

@@ -1,6 +1,6 @@
-"""The pipeline-depth hook (sgemm_cube_compute_stages): every stage count,
-including the no-prefetch single slot, computes the same bits as the default
-pipeline, and those bits meet the parity bar against the oracle."""
+"""The copy/compute overlap hook (sgemm_cube_compute_stages): the setting
+without overlap (stages = 1) computes the same bits as the default pipeline
+(stages = 2), and those bits meet the parity bar against the oracle."""
 import numpy as np
 import pytest
 
