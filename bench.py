@@ -50,14 +50,39 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and with whitespace collapsed, so that a
+    change of comments alone does not count as a change of the kernel."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c == '"':  # string literal (inline asm text): keep verbatim
+            j = i + 1
+            while j < n and text[j] != '"':
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the sources the GEMM kernel is built from (ties a committed
-    HBM-traffic measurement to the kernel it was taken on)."""
+    """Hash of the code (comments excluded) of the sources the GEMM kernel is
+    built from: ties a committed HBM-traffic measurement to the kernel it was
+    taken on."""
     h = hashlib.sha256()
     for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/gemm_fused.hip",
                 "paper_2507_23387_amd/csrc/gemm_common.h", "paper_2507_23387_amd/csrc/internal.h"):
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -143,7 +143,7 @@ def traffic(fetch_dir, write_dir, workload, order, copy_mib):
         f"{4 * M * N / 1e9:.3f} GB written (C); fetch / algorithmic read = "
         f"{fb / alg_read:.1f}x.",
         "",
-        f"Kernel sources hash: {h}",
+        f"Kernel code hash (comments excluded): {h}",
     ]
     return "\n".join(lines)
 
