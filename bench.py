@@ -40,9 +40,9 @@ FP16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12
 THREE_GEMM_PEAK_TFLOPS = FP16_PEAK_TFLOPS / 3
 HBM_PEAK_GBS = 8000.0
 # The MFMA kernel that runs for each order (the elementwise call also launches
-# the narrow kernel, which reads the range flag and returns at once).
-GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true>", "termwise": "gemm_narrow_kernel<1>",
-                "elementwise_cross_first": "gemm_narrow_kernel<3>"}
+# the 256 x 128 fallback kernel, which reads the range flag and returns at once).
+GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true>", "termwise": "gemm_n128_kernel<1>",
+                "elementwise_cross_first": "gemm_n128_kernel<3>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 

@@ -111,22 +111,6 @@ uint32_t next_stamp() {
   return s ? s : g_stamp.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
-// Compute units of the current device, cached per device.
-constexpr int kMaxDevices = 64;
-std::atomic<int> g_cus[kMaxDevices] = {};
-int current_cus() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
-  int n = g_cus[dev].load(std::memory_order_relaxed);
-  if (n <= 0) {
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        n <= 0)
-      n = 256;
-    g_cus[dev].store(n, std::memory_order_relaxed);
-  }
-  return n;
-}
-
 size_t ws_size(int64_t M, int64_t N, int64_t K, bool prescale = false) {
   if (M == 0 || N == 0 || K == 0) return 0;
   return plan_planes(M, N, K, nullptr, prescale).bytes;
@@ -164,11 +148,11 @@ hipError_t compute_from_a(const Planes& p, int64_t M, int64_t N, int64_t K, cons
   if (fused_a_ok(A, lda, K, variant)) {
     const hipError_t e = launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, stream);
     if (e != hipSuccess) return e;
-    return launch_gemm_fallback(p, M, N, C, ldc, scale, current_cus(), stream);
+    return launch_gemm_fallback(p, M, N, C, ldc, scale, stream);
   }
   const hipError_t e = launch_split_a(p, M, K, A, lda, scale, RangeOpts{}, next_stamp(), stream);
   if (e != hipSuccess) return e;
-  return launch_gemm(p, M, N, C, ldc, scale, variant, current_cus(), stream);
+  return launch_gemm(p, M, N, C, ldc, scale, variant, stream);
 }
 
 // Enqueue the whole computation; arguments already validated.  `report`, if
@@ -190,7 +174,7 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
     return SGEMM_CUBE_ERR_HIP;
   if (launch_split_b(p, K, N, B, ldb, scale, opt, next_stamp(), stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
-  if (launch_gemm(p, M, N, C, ldc, scale, variant, current_cus(), stream) != hipSuccess)
+  if (launch_gemm(p, M, N, C, ldc, scale, variant, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   if (opt.prescale && launch_unscale(p, M, N, C, ldc, opt, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
@@ -204,6 +188,7 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
 // freed at the end of a call is reused by the next one instead of going back
 // to the driver at every synchronisation.
 std::mutex g_pool_mu;
+constexpr int kMaxDevices = 64;
 hipMemPool_t g_pools[kMaxDevices] = {};
 
 int get_pool(hipMemPool_t* out) {
@@ -268,8 +253,8 @@ int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
   const Planes p = plan_planes(M, N, K, const_cast<void*>(ws));
   const hipError_t e =
       stages == 0
-          ? launch_gemm(p, M, N, C, ldc, scale, variant_of(accum_order), current_cus(), stream)
-          : launch_gemm_stages(p, M, N, C, ldc, scale, stages, current_cus(), stream);
+          ? launch_gemm(p, M, N, C, ldc, scale, variant_of(accum_order), stream)
+          : launch_gemm_stages(p, M, N, C, ldc, scale, stages, stream);
   return e == hipSuccess ? SGEMM_CUBE_OK : SGEMM_CUBE_ERR_HIP;
 }
 

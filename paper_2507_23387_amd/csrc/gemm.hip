@@ -11,12 +11,12 @@
 //                    elementwise order (Eq. elementwise, Sec. 4.5), one
 //                    accumulator holding s * acc, blocks of one 32-wide
 //                    k-step.
-//   gemm_tw_kernel   256 x 128 tiles, v_mfma_f32_16x16x32_f16: the termwise
-//                    order (Eq. termwise), three accumulators.
+//   gemm_n128_kernel 256 x 128 tiles, v_mfma_f32_16x16x32_f16: the orders
+//                    that need three accumulator sets -- termwise (Eq.
+//                    termwise), the unscaled elementwise fallback (range
+//                    flag set) and the cross-terms-first order (end of
+//                    Sec. 4.5).
 //   gemm_hi_kernel   256 x 256 tiles: HH only, the native-FP16 baseline.
-//   gemm_narrow_kernel  256 x 128 tiles, v_mfma_f32_32x32x16_f16: the
-//                    unscaled elementwise fallback (range flag set) and the
-//                    cross-terms-first order (end of Sec. 4.5).
 // Both elementwise kernels are launched; each reads the range flag first and
 // the one that does not apply returns at once.
 //
@@ -79,7 +79,7 @@ __device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off
 // and C = (s*acc) / s at the end.  s B_hi is formed in registers with
 // v_pk_mul_f16; it is exact because s is a power of two, provided
 // |B_hi| s <= 65504, which the split of B checks (the range flag; when it is
-// set this kernel returns at once and the narrow kernel computes C).  Each
+// set this kernel returns at once and gemm_n128_kernel computes C).  Each
 // block term is summed by the MFMA together with the accumulator, with one
 // rounding, instead of being rounded to FP32 on its own first.
 //
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
   constexpr int kBBase = 2 * kSlotHalves;     // the B slots follow the two A slots
   constexpr int kDmaCols = 4;                 // column blocks that issue the DMAs
   constexpr int kDmaPerCol = 16 / kDmaCols;   // after MFMAs 2, 8, 14, 20 of a block
-  if (range[0] == range[1]) return;  // s B_hi overflows FP16: the narrow kernel runs instead
+  if (range[0] == range[1]) return;  // s B_hi overflows FP16: gemm_n128_kernel runs instead
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
@@ -341,12 +341,25 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Termwise kernel (Eq. termwise) on v_mfma_f32_16x16x32_f16: one 256 x 128
-// tile of C per workgroup, 4 waves of 64 x 128 (one per SIMD).  Three FP32
-// accumulators run over all of K, HH = A_hi B_hi, XA = A_lo B_hi and
-// XB = A_hi B_lo, and the epilogue forms C = (HH + XA / s) + XB / s.  The
-// 3 x 128 accumulator registers of a wave are HH and XA in the 256 AGPRs and
-// XB in VGPRs, every one tied to its registers through mfma16_acc.
+// 256 x 128 tiles on v_mfma_f32_16x16x32_f16 for the orders that need three
+// accumulator sets: one tile of C per workgroup, 4 waves of 64 x 128 (one
+// per SIMD).
+//   kTermwise (Eq. termwise): HH = A_hi B_hi, XA = A_lo B_hi, XB = A_hi B_lo
+//     accumulate over all of K (HH and XA in AGPRs, XB in VGPRs, each
+//     updated once per step) and the epilogue forms C = (HH + XA / s) + XB / s.
+//   kElementwise when the range flag is set (s B_hi overflows FP16, so the
+//     scaled 256 x 256 kernel cannot run): unscaled, blocks of one 32-wide
+//     k-step.  HH goes straight into the accumulator (VGPRs) and XA_g, XB_g
+//     into block sums started from zero; one column block later,
+//     acc = (acc + XA_g / s) + XB_g / s with two v_fma_f32 (1/s is exact).
+//   kCrossFirst (the reordered elementwise accumulation proposed at the end
+//     of Sec. 4.5): per block X_g = XA_g + XB_g (one MFMA chain started from
+//     zero) and HH_g (started from zero); one column block later
+//     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
+// In the block-fold orders the A fragments live in AGPRs (the MFMA reads its
+// A operand from there) so that the accumulators and block sums fit the
+// VGPRs; the fold of column block j runs between the MFMAs of block j+1,
+// 12 MFMAs after the results it reads.
 //
 // The data path is the elementwise kernel's at half the width: LDS holds two
 // A slots (A_hi, A_lo of 256 rows x 32 k: 32 KiB) and two B slots (B_hi,
@@ -356,23 +369,29 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // or two per block, blocks 0-6) and issues 12 DMAs (B stage kt+1, A stage
 // kt+2; two in each of blocks 0-5).  One barrier per step, before the last
 // block, publishes B stage kt+1 and A stage kt+2 and retires B stage kt and
-// A stage kt+1.  Each accumulator is updated once per step (MFMAs on one
-// accumulator are 96 apart).
+// A stage kt+1.
 constexpr int kTwM = 256;
 constexpr int kTwN = 128;
 constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
 constexpr int kTwBSlot = 2 * kTwN * kStep;        // halves: B_hi, B_lo of one step
 constexpr size_t kTwLdsBytes = static_cast<size_t>(2) * (kTwASlot + kTwBSlot) * 2;  // 96 KiB
 
-__global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
+template <int V>
+__global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
-    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo, int Kp, int tiles_m,
-    int tiles_n, float* __restrict__ C, int64_t ldc, int M, int N, float inv_s) {
+    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
+    const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
+    float* __restrict__ C, int64_t ldc, int M, int N, float inv_s) {
+  static_assert(V == kTermwise || V == kElementwise || V == kCrossFirst, "n128 variants");
+  constexpr bool kFold = V != kTermwise;
   constexpr int kRows = 4;                   // 16-row blocks per wave
   constexpr int kCols = 8;                   // 16-column blocks per wave
-  constexpr int kAPlane = kTwM * kStep;      // one A plane of one step: 8 tiles... 16 KiB
+  constexpr int kAPlane = kTwM * kStep;      // one A plane of one step: 16 KiB
   constexpr int kBPlane = kTwN * kStep;      // one B plane of one step: 8 KiB
   constexpr int kBBase = 2 * kTwASlot;       // the B slots follow the two A slots
+  if constexpr (V == kElementwise) {
+    if (range[0] != range[1]) return;  // the scaled 256 x 256 kernel handles this case
+  }
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
@@ -428,11 +447,22 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
                                            b_off[j & 1] + j * 16 * kSlice);
   };
 
-  floatx4 hh[kRows][kCols], xa[kRows][kCols], xb[kRows][kCols];
+  // Termwise: hh, xa, xb.  Block folds: acc (= hh) and the block sums t1, t2
+  // of the current and the previous column block (index: block parity).
+  floatx4 hh[kRows][kCols], xa[kFold ? 1 : kRows][kFold ? 1 : kCols],
+      xb[kFold ? 1 : kRows][kFold ? 1 : kCols], t1[2][kRows], t2[2][kRows];
 #pragma unroll
-  for (int i = 0; i < kRows; ++i)
+  for (int i = 0; i < kRows; ++i) {
 #pragma unroll
-    for (int j = 0; j < kCols; ++j) hh[i][j] = xa[i][j] = xb[i][j] = floatx4{};
+    for (int j = 0; j < kCols; ++j) hh[i][j] = floatx4{};
+    t1[0][i] = t1[1][i] = t2[0][i] = t2[1][i] = floatx4{};
+  }
+  if constexpr (!kFold) {
+#pragma unroll
+    for (int i = 0; i < kRows; ++i)
+#pragma unroll
+      for (int j = 0; j < kCols; ++j) xa[i][j] = xb[i][j] = floatx4{};
+  }
 
   static_for<8>([&](auto n) { dma_a(0, decltype(n)::value); });
   static_for<8>([&](auto n) { dma_a(1, decltype(n)::value); });
@@ -449,13 +479,32 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
   bl[0] = rd_b(0, 1, 0);
   lds_barrier();  // A slot 0 is refilled (stage 2) during step 0
 
-  // Column block j issues HH(., j), XA(., j), XB(., j).  After MFMA m of a
-  // block: m = 1, 7 read the next A fragments, m = 3, 9 of blocks 0-5 issue
-  // the DMAs.
+  // The fold of column block jp (block sums of parity cp) for rows and
+  // elements q = 4 i + e in [q0, q1).
+  auto fold = [&](int jp, int cp, int q0, int q1) {
+#pragma unroll
+    for (int q = q0; q < q1; ++q) {
+      const int i = q >> 2, e = q & 3;
+      if constexpr (V == kElementwise) {
+        float v = __builtin_fmaf(t1[cp][i][e], inv_s, hh[i][jp][e]);
+        hh[i][jp][e] = __builtin_fmaf(t2[cp][i][e], inv_s, v);
+      } else {
+        hh[i][jp][e] += __builtin_fmaf(t1[cp][i][e], inv_s, t2[cp][i][e]);
+      }
+    }
+  };
+
+  // Column block j issues its 12 MFMAs: termwise HH(., j), XA(., j),
+  // XB(., j); elementwise HH into acc, XA_g, XB_g; cross-first HH_g, XA_g,
+  // then XB_g chained onto XA_g.  After MFMA m of a block: m = 1, 7 read the
+  // next A fragments, m = 3, 9 of blocks 0-5 issue the DMAs, and in the
+  // block-fold orders every MFMA is followed by 1-2 of the 16 folds of the
+  // previous column block.
   auto step = [&](int kt, half8 (&ah)[kRows], half8 (&al)[kRows], half8 (&nh)[kRows],
                   half8 (&nl)[kRows]) {
     static_for<kCols>([&](auto J) {
       constexpr int j = decltype(J)::value, c = j & 1;
+      constexpr int jp = (j + kCols - 1) % kCols;  // the block folded now
       if constexpr (j == kCols - 1) {
         wait_vmcnt<0>();
         lds_barrier();
@@ -470,13 +519,30 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
       constexpr int rb = (8 * j + 6) / 7, re = (8 * (j + 1) + 6) / 7;
       static_for<3 * kRows>([&](auto Mc) {
         constexpr int m = decltype(Mc)::value, g = m / kRows, i = m % kRows;
-        if constexpr (g == 0)
-          mfma16_acc(hh[i][j], ah[i], bh[c]);
-        else if constexpr (g == 1)
-          mfma16_acc(xa[i][j], al[i], bh[c]);
-        else
-          mfma16_vacc(xb[i][j], ah[i], bl[c]);
+        if constexpr (V == kTermwise) {
+          if constexpr (g == 0)
+            mfma16_acc(hh[i][j], ah[i], bh[c]);
+          else if constexpr (g == 1)
+            mfma16_acc(xa[i][j], al[i], bh[c]);
+          else
+            mfma16_vacc(xb[i][j], ah[i], bl[c]);
+        } else if constexpr (V == kElementwise) {
+          if constexpr (g == 0)
+            mfma16_va_acc(hh[i][j], ah[i], bh[c]);
+          else if constexpr (g == 1)
+            mfma16_va_new(t1[c][i], al[i], bh[c]);
+          else
+            mfma16_va_new(t2[c][i], ah[i], bl[c]);
+        } else {
+          if constexpr (g == 0)
+            mfma16_va_new(t2[c][i], ah[i], bh[c]);
+          else if constexpr (g == 1)
+            mfma16_va_new(t1[c][i], al[i], bh[c]);
+          else
+            mfma16_va_acc(t1[c][i], ah[i], bl[c]);
+        }
         SCHED_FENCE();
+        if constexpr (kFold) fold(jp, c ^ 1, (16 * m) / 12, (16 * (m + 1)) / 12);
         if constexpr (j < kCols - 1 && (m == 1 || m == 7)) {
           constexpr int r = rb + m / 6;
           if constexpr (r < re) {
@@ -497,209 +563,19 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_tw_kernel(
   }
   wait_vmcnt<0>();
   mfma_drain();
+  if constexpr (kFold) fold(kCols - 1, 1, 0, 4 * kRows);
 
   const int col0 = tn * kTwN + (lane & 15);
   const int row0 = tm * kTwM + w * 64 + (lane >> 4) * 4;
   const bool full = (tm + 1) * kTwM <= M && (tn + 1) * kTwN <= N;
   store_tile16<kRows, kCols>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
-    return __builtin_fmaf(xb[i][j][r], inv_s, __builtin_fmaf(xa[i][j][r], inv_s, hh[i][j][r]));
+    if constexpr (kFold) {
+      return hh[i][j][r];
+    } else {
+      return __builtin_fmaf(xb[i][j][r], inv_s, __builtin_fmaf(xa[i][j][r], inv_s, hh[i][j][r]));
+    }
   });
 }
-
-// ---------------------------------------------------------------------------
-// 256 x 128 tiles on v_mfma_f32_32x32x16_f16, 8 waves of 64 x 64 (two per
-// SIMD), three 64-register accumulator sets in VGPRs:
-//   kElementwise when the range flag is set: unscaled, blocks of two k-steps
-//     (32): HH goes straight into the accumulator, XA_g and XB_g into block
-//     sums started from zero, and acc = (acc + XA_g / s) + XB_g / s with two
-//     v_fma_f32 at the end of each block (1/s is exact).
-//   kCrossFirst (the reordered elementwise accumulation proposed at the end
-//     of Sec. 4.5): per block g of two k-steps the cross products are summed
-//     first, X_g = XA_g + XB_g (one MFMA chain), HH_g separately, and
-//     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
-// Stages of one 16-k slice of the four planes go into a 4-slot LDS ring.  In
-// k-step kt the fragments of step kt+1 are read while the MFMAs of step kt
-// run: each fragment register is reloaded as soon as its last MFMA of the
-// step has been issued, and the DMAs for stage kt+4 are spread between the
-// MFMA groups.  One s_barrier per step publishes stage kt+1 and retires the
-// slot of stage kt.  A persistent grid of one workgroup per compute unit
-// walks the tiles.
-constexpr int kNarrowM = 256;
-constexpr int kNarrowN = 128;
-constexpr int kNarrowThreads = 512;
-constexpr int kNarrowStages = 4;
-constexpr size_t kNarrowLdsBytes =
-    static_cast<size_t>(kNarrowStages) * 2 * (kNarrowM + kNarrowN) * kSlice * 2;
-
-template <int V>
-__global__ __launch_bounds__(kNarrowThreads, 1) void gemm_narrow_kernel(
-    const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
-    const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
-    const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
-    float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
-  static_assert(V == kElementwise || V == kCrossFirst, "narrow kernel variants");
-  constexpr int S = kNarrowStages;
-  constexpr int kAHalves = kNarrowM * kSlice;  // A plane slot: two tiles
-  constexpr int kBHalves = kNarrowN * kSlice;  // B plane slot: one tile
-  constexpr int kAH = 0, kAL = kAHalves, kBH = 2 * kAHalves, kBL = 2 * kAHalves + kBHalves;
-  constexpr int kStageHalves = 2 * (kAHalves + kBHalves);
-  constexpr int kDma = 3;  // 24 blocks of 1 KiB per stage over 8 waves
-  constexpr int kSub = 2;
-  if constexpr (V == kElementwise) {
-    if (range[0] != range[1]) return;  // the scaled wide kernel handles this case
-  }
-  extern __shared__ __align__(16) uint16_t lds[];
-
-  const int lane = threadIdx.x & 63;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm = w >> 1, wn = w & 1;
-  // Persistent grid: each workgroup walks tiles blockIdx.x, + gridDim.x, ...
-  for (int tile = blockIdx.x; tile < tiles_m * tiles_n; tile += gridDim.x) {
-    int tm, tn;
-    tile_of<8>(tile, tiles_m, tiles_n, tm, tn);
-    // Every wave is done with the previous tile's LDS before it is refilled.
-    lds_barrier();
-    const int64_t slices = Kp / kSlice;
-    const int ktiles = static_cast<int>(slices);
-    const int64_t panel_stride = slices * kTileHalves;
-
-    // Wave w copies block w of A_hi and of A_lo (8 blocks each: two tiles of
-    // four) and block w of the eight blocks of B_hi and B_lo.
-    const uint16_t* src[3] = {
-        a_hi + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
-        a_lo + (2 * tm + (w >> 2)) * panel_stride + (w & 3) * 512 + lane * 8,
-        (w < 4 ? b_hi : b_lo) + tn * panel_stride + (w & 3) * 512 + lane * 8};
-    const int dst_off[3] = {kAH + w * 512, kAL + w * 512, (w < 4 ? kBH : kBL) + (w & 3) * 512};
-    const unsigned lds_base = lds_address(lds);
-    auto dma_one = [&](int kt, int n) {
-      const int ktc = min(kt, ktiles - 1);
-      dma16(src[n] + static_cast<int64_t>(ktc) * kTileHalves,
-            lds_base + ((kt % S) * kStageHalves + dst_off[n]) * 2);
-    };
-
-    const int fr = lane & 31, fk = lane >> 5;
-    int aoff[kSub], boff[kSub];
-  #pragma unroll
-    for (int i = 0; i < kSub; ++i) {
-      aoff[i] = frag_offset(wm * 64 + i * 32 + fr, fk);
-      boff[i] = frag_offset(wn * 64 + i * 32 + fr, fk);
-    }
-    auto rd = [&](int kt, int slot, int off) -> half8 {
-      return *reinterpret_cast<const half8*>(lds + (kt % S) * kStageHalves + slot + off);
-    };
-    const floatx16 zero = {};
-    floatx16 acc[kSub][kSub], xa[kSub][kSub], xb[kSub][kSub];
-  #pragma unroll
-    for (int i = 0; i < kSub; ++i)
-  #pragma unroll
-      for (int j = 0; j < kSub; ++j) acc[i][j] = xa[i][j] = xb[i][j] = zero;
-    half8 ah[kSub], al[kSub], bh[kSub], bl[kSub];
-
-  #pragma unroll
-    for (int st = 0; st < S; ++st)
-  #pragma unroll
-      for (int n = 0; n < kDma; ++n) dma_one(st, n);
-    wait_vmcnt<(S - 1) * kDma>();
-    lds_barrier();
-  #pragma unroll
-    for (int i = 0; i < kSub; ++i) {
-      ah[i] = rd(0, kAH, aoff[i]);
-      al[i] = rd(0, kAL, aoff[i]);
-      bh[i] = rd(0, kBH, boff[i]);
-      bl[i] = rd(0, kBL, boff[i]);
-    }
-
-    // One k-step: XA, then HH, then XB; each fragment is reloaded with step
-    // kt+1 once its last MFMA of the step is issued.  `first` marks the first
-    // step of a block (block sums restart), `last` its end (fold).  Register
-    // sets: elementwise fallback acc = running sum, xa = XA_g, xb = XB_g;
-    // cross-first acc = running sum, xa = X_g = XA_g + XB_g, xb = HH_g.
-    constexpr bool kBlocks = true;
-    auto step = [&](int kt, bool first, bool last) {
-      const int nk = kt + 1;
-#pragma unroll
-      for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j)
-          xa[i][j] = mfma32(al[i], bh[j], (kBlocks && first) ? zero : xa[i][j]);
-      SCHED_FENCE();
-      wait_vmcnt<(S - 2) * kDma>();
-      lds_barrier();
-#pragma unroll
-      for (int i = 0; i < kSub; ++i) al[i] = rd(nk, kAL, aoff[i]);
-      dma_one(kt + S, 0);
-      SCHED_FENCE();
-#pragma unroll
-      for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-          if constexpr (V == kCrossFirst)
-            xb[i][j] = mfma32(ah[i], bh[j], first ? zero : xb[i][j]);
-          else
-            acc[i][j] = mfma32(ah[i], bh[j], acc[i][j]);
-        }
-      SCHED_FENCE();
-#pragma unroll
-      for (int j = 0; j < kSub; ++j) bh[j] = rd(nk, kBH, boff[j]);
-      dma_one(kt + S, 1);
-      SCHED_FENCE();
-#pragma unroll
-      for (int i = 0; i < kSub; ++i)
-#pragma unroll
-        for (int j = 0; j < kSub; ++j) {
-          if constexpr (V == kCrossFirst)
-            xa[i][j] = mfma32(ah[i], bl[j], xa[i][j]);
-          else
-            xb[i][j] = mfma32(ah[i], bl[j], (kBlocks && first) ? zero : xb[i][j]);
-        }
-      SCHED_FENCE();
-#pragma unroll
-      for (int i = 0; i < kSub; ++i) {
-        ah[i] = rd(nk, kAH, aoff[i]);
-        bl[i] = rd(nk, kBL, boff[i]);
-      }
-      dma_one(kt + S, 2);
-      SCHED_FENCE();
-      if constexpr (V == kElementwise) {
-        if (last) {
-          // End of block g: acc = (acc + XA_g / s) + XB_g / s.
-#pragma unroll
-          for (int i = 0; i < kSub; ++i)
-#pragma unroll
-            for (int j = 0; j < kSub; ++j)
-#pragma unroll
-              for (int e = 0; e < 16; ++e) {
-                acc[i][j][e] = __builtin_fmaf(xa[i][j][e], inv_s, acc[i][j][e]);
-                acc[i][j][e] = __builtin_fmaf(xb[i][j][e], inv_s, acc[i][j][e]);
-              }
-        }
-      } else if constexpr (V == kCrossFirst) {
-        if (last) {
-          // End of block g: acc = acc + (X_g / s + HH_g).
-#pragma unroll
-          for (int i = 0; i < kSub; ++i)
-#pragma unroll
-            for (int j = 0; j < kSub; ++j)
-#pragma unroll
-              for (int e = 0; e < 16; ++e)
-                acc[i][j][e] += __builtin_fmaf(xa[i][j][e], inv_s, xb[i][j][e]);
-        }
-      }
-    };
-    for (int kt = 0; kt < ktiles; kt += 2) {
-      step(kt, true, false);
-      step(kt + 1, false, true);
-    }
-    wait_vmcnt<0>();
-
-    const int col0 = tn * kNarrowN + wn * 64 + (lane & 31);
-    const int row0 = tm * kNarrowM + wm * 64 + (lane >> 5) * 4;
-    const bool full = (tm + 1) * kNarrowM <= M && (tn + 1) * kNarrowN <= N;
-    store_tile<kSub, kSub>(C, ldc, M, N, row0, col0, full,
-                           [&](int i, int j, int r) { return acc[i][j][r]; });
-  }
-}
-
 
 template <bool kPrefetch>
 hipError_t launch_el(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
@@ -729,62 +605,45 @@ hipError_t launch_hi(const Planes& p, int64_t M, int64_t N, float* C, int64_t ld
   return hipGetLastError();
 }
 
-hipError_t launch_tw(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                     hipStream_t stream) {
+template <int V>
+hipError_t launch_n128(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
+                       hipStream_t stream) {
   static std::atomic<bool> done[kMaxDevices];
-  const hipError_t attr = set_lds(&gemm_tw_kernel, kTwLdsBytes, done);
+  const hipError_t attr = set_lds(&gemm_n128_kernel<V>, kTwLdsBytes, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kTwM);
   const int tiles_n = static_cast<int>(p.Np / kTwN);
-  hipLaunchKernelGGL(gemm_tw_kernel, dim3(tiles_m * tiles_n), dim3(kWideThreads), kTwLdsBytes,
-                     stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, static_cast<int>(p.Kp), tiles_m,
-                     tiles_n, C, ldc, static_cast<int>(M), static_cast<int>(N), 1.0f / s);
-  return hipGetLastError();
-}
-
-template <int V>
-hipError_t launch_narrow(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                         int cus, hipStream_t stream) {
-  static std::atomic<bool> done[kMaxDevices];
-  const hipError_t attr = set_lds(&gemm_narrow_kernel<V>, kNarrowLdsBytes, done);
-  if (attr != hipSuccess) return attr;
-  const int tiles_m = static_cast<int>(p.Mp / kNarrowM);
-  const int tiles_n = static_cast<int>(p.Np / kNarrowN);
-  // One workgroup per compute unit (the kernel's occupancy), rounded to the
-  // 8 XCDs; fewer when there are fewer tiles.
-  const int grid = static_cast<int>(
-      std::min<int64_t>(static_cast<int64_t>(tiles_m) * tiles_n, std::max(8, cus / 8 * 8)));
-  hipLaunchKernelGGL(gemm_narrow_kernel<V>, dim3(grid), dim3(kNarrowThreads),
-                     kNarrowLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
+  hipLaunchKernelGGL((gemm_n128_kernel<V>), dim3(tiles_m * tiles_n), dim3(kWideThreads),
+                     kTwLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
                      static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
-                     static_cast<int>(N), s, 1.0f / s);
+                     static_cast<int>(N), 1.0f / s);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                       float scale, int variant, int cus, hipStream_t stream) {
+                       float scale, int variant, hipStream_t stream) {
   switch (variant) {
     case kElementwise: {
       const hipError_t e = launch_el<true>(p, M, N, C, ldc, scale, stream);
       if (e != hipSuccess) return e;
-      return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
+      return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
     }
-    case kTermwise: return launch_tw(p, M, N, C, ldc, scale, stream);
-    case kCrossFirst: return launch_narrow<kCrossFirst>(p, M, N, C, ldc, scale, cus, stream);
+    case kTermwise: return launch_n128<kTermwise>(p, M, N, C, ldc, scale, stream);
+    case kCrossFirst: return launch_n128<kCrossFirst>(p, M, N, C, ldc, scale, stream);
     case kHiOnly: return launch_hi(p, M, N, C, ldc, stream);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                                float scale, int cus, hipStream_t stream) {
-  return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
+                                float scale, hipStream_t stream) {
+  return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
 }
 
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                              float scale, int stages, int cus, hipStream_t stream) {
+                              float scale, int stages, hipStream_t stream) {
   hipError_t e = hipSuccess;
   switch (stages) {
     case 1: e = launch_el<false>(p, M, N, C, ldc, scale, stream); break;
@@ -792,7 +651,7 @@ hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, i
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;
-  return launch_narrow<kElementwise>(p, M, N, C, ldc, scale, cus, stream);
+  return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
 }
 
 }  // namespace sgc

@@ -12,15 +12,7 @@ namespace sgc {
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
-
-// D(32x32) = A(32x16) B(16x32) + C.  Lane l supplies A row l%32 and B column
-// l%32 with the 8 consecutive k values 8*(l/32) .. 8*(l/32)+7 of the 16-wide
-// step; D element (row 8*(r/4) + 4*(l/32) + r%4, column l%32) is in register r.
-__device__ __forceinline__ floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
-}
 
 // One 64-lane LDS DMA: lane l copies 16 bytes from g into LDS byte address
 // lds_addr + 16 * l (the instruction takes the LDS base from M0, which the
@@ -57,11 +49,6 @@ __device__ __forceinline__ void lds_barrier() {
 
 // Keeps the instruction groups of the schedule in program order.
 #define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
-
-// Offset (halves) of the fragment of LDS row r for k chunk fk (0 or 1).
-__device__ __forceinline__ int frag_offset(int r, int fk) {
-  return r * kSlice + ((fk ^ tile_swizzle(r)) << 3);
-}
 
 // LDS byte address of the dynamic shared-memory base (the M0 operand of the
 // DMA): cast the generic pointer to the LDS address space, then to int.
@@ -109,38 +96,6 @@ __device__ __forceinline__ bool tile_of_block(int index, int tiles_m, int tiles_
   return true;
 }
 
-// Store a wave's accumulators: register r of MFMA tile (i, j) holds row
-// 8*(r/4) + 4*(l/32) + r%4 and column l%32 of that 32 x 32 tile.  `value`
-// maps (i, j, r) to the float to store.  Tiles entirely inside C take the
-// unmasked path; row offsets are wave-uniform multiples of ldc.
-template <int kSubM, int kSubN, typename F>
-__device__ __forceinline__ void store_tile(float* __restrict__ C, int64_t ldc, int M, int N,
-                                           int row0, int col0, bool full, F value) {
-  float* const base = C + static_cast<int64_t>(row0) * ldc + col0;
-  if (full) {
-#pragma unroll
-    for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float* const p = base + static_cast<int64_t>(i * 32 + (r >> 2) * 8 + (r & 3)) * ldc;
-#pragma unroll
-        for (int j = 0; j < kSubN; ++j) p[j * 32] = value(i, j, r);
-      }
-  } else {
-#pragma unroll
-    for (int i = 0; i < kSubM; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int rr = i * 32 + (r >> 2) * 8 + (r & 3);
-        float* const p = base + static_cast<int64_t>(rr) * ldc;
-#pragma unroll
-        for (int j = 0; j < kSubN; ++j)
-          if (row0 + rr < M && col0 + j * 32 < N) p[j * 32] = value(i, j, r);
-      }
-  }
-}
-
-
 // D(16x16) = A(16x32) B(32x16) + C.  Lane l supplies A row l%16 and B column
 // l%16 with the 8 consecutive k values 8*(l/16) .. 8*(l/16)+7 of the 32-wide
 // step; D element (row 4*(l/16) + r, column l%16) is in register r.
@@ -178,6 +133,17 @@ __device__ __forceinline__ half8 pk_scale(const half8& x, uint32_t s2) {
 // The same with the accumulator tied to a VGPR quad.
 __device__ __forceinline__ void mfma16_vacc(floatx4& acc, const half8& a, const half8& b) {
   asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));
+}
+
+// acc += A B with the accumulator tied to a VGPR quad and the A operand read
+// from AGPRs (the block-fold kernels keep their A fragments there).
+__device__ __forceinline__ void mfma16_va_acc(floatx4& acc, const half8& a, const half8& b) {
+  asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(acc) : "a"(a), "v"(b));
+}
+
+// out = A B (accumulator input zero) into a fresh VGPR quad, A from AGPRs.
+__device__ __forceinline__ void mfma16_va_new(floatx4& out, const half8& a, const half8& b) {
+  asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, 0" : "=&v"(out) : "a"(a), "v"(b));
 }
 
 // Wait states after the last mfma16_acc before its accumulators are read.

@@ -141,17 +141,16 @@ hipError_t launch_unscale(const Planes& p, int64_t M, int64_t N, float* C, int64
 // (0 when `empty`, i.e. no split ran).
 hipError_t launch_range_report(const Planes& p, bool empty, uint32_t* out, hipStream_t stream);
 
-// Enqueue the MFMA GEMM on prepared planes.  `cus` is the device's compute
-// unit count (sizes the persistent grid of the 256 x 128 kernel).
+// Enqueue the MFMA GEMM on prepared planes.
 hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                       float scale, int variant, int cus, hipStream_t stream);
+                       float scale, int variant, hipStream_t stream);
 
 // The elementwise GEMM with the copies of the 256 x 256 kernel overlapped
 // with its MFMAs (stages = 2, the library's default) or issued and waited for
 // at the end of each step (stages = 1), for the pipeline ablation.  The
 // fallback kernel (range flag set) keeps its own pipeline.
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                              float scale, int stages, int cus, hipStream_t stream);
+                              float scale, int stages, hipStream_t stream);
 
 // Elementwise GEMM that reads A as FP32 and splits it in registers
 // (gemm_fused.hip), on a workspace whose B planes and range flag were written
@@ -165,15 +164,15 @@ hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
 // The unscaled elementwise kernel alone; it computes C only when the range
 // flag is set (and returns at once otherwise).
 hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                                float scale, int cus, hipStream_t stream);
+                                float scale, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);
 
-// The elementwise k-block of the scaled kernel (one 16 x 16 x 32 MFMA k-step),
-// and of the fallback kernel used when the range flag is set and of the
-// cross-terms-first order (two 32 x 32 x 16 MFMA k-steps).
+// The elementwise k-block of the scaled kernel, of the fallback kernel used
+// when the range flag is set and of the cross-terms-first order: one
+// 16 x 16 x 32 MFMA k-step.
 constexpr int kBlockScaled = 2 * kSlice;
 constexpr int kBlockFallback = 2 * kSlice;
 
