@@ -358,8 +358,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 //     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
 // In the block-fold orders the A fragments live in AGPRs (the MFMA reads its
 // A operand from there) so that the accumulators and block sums fit the
-// VGPRs; the fold of column block j runs between the MFMAs of block j+1,
-// 12 MFMAs after the results it reads.
+// VGPRs; the fold of column block j runs between the MFMAs of block j+1, at
+// least 8 MFMAs after the results it reads.
 //
 // The data path is the elementwise kernel's at half the width: LDS holds two
 // A slots (A_hi, A_lo of 256 rows x 32 k: 32 KiB) and two B slots (B_hi,
@@ -498,8 +498,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   // XB(., j); elementwise HH into acc, XA_g, XB_g; cross-first HH_g, XA_g,
   // then XB_g chained onto XA_g.  After MFMA m of a block: m = 1, 7 read the
   // next A fragments, m = 3, 9 of blocks 0-5 issue the DMAs, and in the
-  // block-fold orders every MFMA is followed by 1-2 of the 16 folds of the
-  // previous column block.
+  // block-fold orders MFMAs 3-11 are each followed by 1-2 of the 16 folds of
+  // the previous column block.
   auto step = [&](int kt, half8 (&ah)[kRows], half8 (&al)[kRows], half8 (&nh)[kRows],
                   half8 (&nl)[kRows]) {
     static_for<kCols>([&](auto J) {
@@ -542,7 +542,9 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
             mfma16_va_acc(t1[c][i], ah[i], bl[c]);
         }
         SCHED_FENCE();
-        if constexpr (kFold) fold(jp, c ^ 1, (16 * m) / 12, (16 * (m + 1)) / 12);
+        // Folds after MFMAs 3-11: every sum read here was written at least 8
+        // MFMAs earlier (XB_g of row i, the last, by MFMA 8 + i of block jp).
+        if constexpr (kFold && m >= 3) fold(jp, c ^ 1, (16 * (m - 3)) / 9, (16 * (m - 2)) / 9);
         if constexpr (j < kCols - 1 && (m == 1 || m == 7)) {
           constexpr int r = rb + m / 6;
           if constexpr (r < re) {

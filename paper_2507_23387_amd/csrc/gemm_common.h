@@ -106,11 +106,14 @@ __device__ __forceinline__ floatx4 mfma16(const half8& a, const half8& b, const 
 // acc += A B on v_mfma_f32_16x16x32_f16 (operands as for mfma16), with the
 // accumulator tied to one AGPR quad ("+a") so that the register allocator
 // keeps every accumulator in place across the main loop.  The compiler does
-// not see an MFMA here, so the callers keep the MFMA hazards themselves:
-// dependent MFMAs on one accumulator are at least 8 MFMAs apart, operand
-// registers are written at least 8 MFMAs before or after they are read, and
-// the accumulators are read by other instructions only after
-// mfma_drain().
+// not see an MFMA here, so the callers keep the MFMA hazards themselves, by
+// distance in the instruction stream (one of these MFMAs occupies the
+// matrix pipe 16 cycles): an MFMA that reads another's result as its C
+// operand comes at least 4 MFMAs after it (8 in the 256 x 256 kernels); a
+// VALU instruction that reads an MFMA result comes at least 8 MFMAs after
+// it, or after mfma_drain(); VALU results an MFMA reads are written at
+// least 8 MFMAs before it; and an operand register is rewritten (by an LDS
+// read) no earlier than one MFMA after its last reader was issued.
 __device__ __forceinline__ void mfma16_acc(floatx4& acc, const half8& a, const half8& b) {
   asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
