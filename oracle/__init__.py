@@ -18,9 +18,11 @@ Functions and what pins them (see tests/test_oracle_*.py):
   Sec. 4.5.  Pinned by exact recovery on constructed inputs, the exact value of
   the dropped lo*lo term (Eq. recover_eqn), Eq. ll_bound, Eq. truncation and
   Eq. main_bound by brute force in exact rationals, and textbook reductions
-  (FP16-exact inputs, one block).  ELEMENTWISE_CROSS_FIRST has no printed
-  bound; beyond the shared truncation and a derived summation bound its
-  parity is unpinned.
+  (FP16-exact inputs, one block).  ELEMENTWISE and ELEMENTWISE_CROSS_FIRST
+  have no printed bound: each is also pinned, by brute force in exact
+  rationals, to the standard summation bound gamma_d * sum|terms| around the
+  exact three-term sum, d the order's longest rounding chain
+  (bounds.elementwise_depth, bounds.cross_first_depth).
 * ``prescale_exponents`` / ``sgemm_prescaled`` / ``range_classes``: the
   range extensions the paper names without fixing a rule (exponent
   management of the high part, Sec. 4.2; input-dependent scaling and an

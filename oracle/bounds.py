@@ -61,6 +61,17 @@ def elementwise_depth(K: int, kb: int) -> int:
     return (min(kb, K) - 1) + 3 * nblocks
 
 
+def cross_first_depth(K: int, kb: int) -> int:
+    """Same count for the cross-terms-first order (end of Sec. 4.5): up to
+    kb-1 inside a block sum, then X_g = XA_g + XB_g, then X_g / s + HH_g (the
+    division by the power of two s is exact), then the addition to the
+    running sum in the term's own block and one more in each later block."""
+    if K == 0:
+        return 0
+    nblocks = -(-K // kb)
+    return (min(kb, K) - 1) + 2 + nblocks
+
+
 def termwise_depth(K: int, kb: int) -> int:
     """Same count for the blocked termwise order: up to kb-1 inside the block,
     up to G more in the stream sum over blocks, then the two final additions."""

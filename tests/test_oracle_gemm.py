@@ -110,8 +110,9 @@ def test_truncation_and_main_bound_brute_force(case):
         of the three computed terms built from the oracle's split;
       Eq. ll_bound: |R_A R_B| / s^2 <= u16^2 (1+u16)^2 |A||B|;
       Eq. main_bound: the termwise result satisfies |AB - C| <= coef(k) |A||B|;
-      the elementwise result satisfies |S - C| <= gamma_d sum|terms| with d
-        its longest rounding chain (the paper prints no elementwise bound)."""
+      the elementwise and the cross-terms-first results satisfy
+        |S - C| <= gamma_d sum|terms| with d the order's longest rounding
+        chain (the paper prints no bound for either)."""
     rng = np.random.default_rng(100 + case)
     M, N, K = 4, 5, [1, 3, 8, 8, 16, 5][case]
     kb = [1, 2, 3, 8, 4, 64][case]
@@ -139,9 +140,11 @@ def test_truncation_and_main_bound_brute_force(case):
               for j in range(N)] for i in range(M)]
     Ct = oracle.sgemm(A, B, s, "termwise", kb=kb)
     Ce = oracle.sgemm(A, B, s, "elementwise", kb=kb)
+    Cc = oracle.sgemm(A, B, s, "elementwise_cross_first", kb=kb)
     coef = bounds.main_bound_coef(K)
     d = bounds.elementwise_depth(K, kb)
     ge = bounds.gamma(d)
+    gc = bounds.gamma(bounds.cross_first_depth(K, kb))
     for i in range(M):
         for j in range(N):
             T = AB[i][j] - S[i][j]
@@ -149,6 +152,7 @@ def test_truncation_and_main_bound_brute_force(case):
             assert abs(LL[i][j]) <= bounds.LL_COEF * absAB[i][j]
             assert abs(AB[i][j] - Fraction(float(Ct[i, j]))) <= coef * absAB[i][j]
             assert abs(S[i][j] - Fraction(float(Ce[i, j]))) <= ge * terms[i][j]
+            assert abs(S[i][j] - Fraction(float(Cc[i, j]))) <= gc * terms[i][j]
 
 
 def test_main_bound_at_256_cubed_against_fp64():
