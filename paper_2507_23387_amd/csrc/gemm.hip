@@ -367,9 +367,10 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // in registers and streams B one 16-column block at a time, one block ahead;
 // during step kt it reads the A fragments of step kt+1 into a second set (one
 // or two per block, blocks 0-6) and issues 12 DMAs (B stage kt+1, A stage
-// kt+2; two in each of blocks 0-5).  One barrier per step, before the last
-// block, publishes B stage kt+1 and A stage kt+2 and retires B stage kt and
-// A stage kt+1.
+// kt+2; three in each of blocks 0-3, so that they land before the barrier:
+// spread two per block over blocks 0-5 they left the block-fold orders 5-6 %
+// slower).  One barrier per step, before the last block, publishes B stage
+// kt+1 and A stage kt+2 and retires B stage kt and A stage kt+1.
 constexpr int kTwM = 256;
 constexpr int kTwN = 128;
 constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
@@ -497,7 +498,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   // Column block j issues its 12 MFMAs: termwise HH(., j), XA(., j),
   // XB(., j); elementwise HH into acc, XA_g, XB_g; cross-first HH_g, XA_g,
   // then XB_g chained onto XA_g.  After MFMA m of a block: m = 1, 7 read the
-  // next A fragments, m = 3, 9 of blocks 0-5 issue the DMAs, and in the
+  // next A fragments, m = 2, 6, 10 of blocks 0-3 issue the DMAs, and in the
   // block-fold orders MFMAs 3-11 are each followed by 1-2 of the 16 folds of
   // the previous column block.
   auto step = [&](int kt, half8 (&ah)[kRows], half8 (&al)[kRows], half8 (&nh)[kRows],
@@ -554,7 +555,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
               nl[r - kRows] = rd_a(kt + 1, 1, r - kRows);
           }
         }
-        if constexpr (j < 6 && (m == 3 || m == 9)) dma(kt, 2 * j + m / 6);
+        if constexpr (j < 4 && m % 4 == 2) dma(kt, 3 * j + m / 4);
         SCHED_FENCE();
       });
     });
