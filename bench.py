@@ -14,7 +14,9 @@ stream can time the dominant GEMM kernel inside the timed region.
 Prints ONE JSON line.  `value` = 2MNK / t (FP32-equivalent TFLOP/s, Sec. 6.1);
 `roofline` prices the GEMM kernel's 6MNK FP16 MFMA flops against the dense
 FP16 MFMA peak; `cpu_baseline` times the CPU oracle on a bounded row sample of
-the same workload on this host.
+the same workload on this host; `context` times, outside the timed region and
+on the same operands, the native-FP16 baseline call of this library and the
+vendor FP32 and FP16 GEMMs (torch.matmul), as reference points only.
 """
 from __future__ import annotations
 
@@ -148,6 +150,61 @@ def cpu_baseline(A, B, w, scale, order, target_s: float):
     }
 
 
+def _timed_ms(fn, stream, reps: int) -> float:
+    """Mean duration of fn() over `reps` calls, HIP events on `stream`."""
+    import torch
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def context_gemms(sgc, dA, dB, A, B, rows, stream, with_errors: bool):
+    """Reference points on the same operands, outside the timed region: the
+    native-FP16 MFMA baseline of this library (sgemm_cube_hgemm: FP32 in,
+    fl16 conversion + HH-only GEMM), the vendor FP32 GEMM (torch.matmul on
+    FP32, the call SGEMM-cube stands in for) and the vendor FP16 GEMM on
+    operands already converted to FP16 (conversion not timed)."""
+    import torch
+    M, K = dA.shape
+    N = dB.shape[1]
+    flops = 2.0 * M * N * K
+    out = {}
+    Ch = torch.empty((M, N), dtype=torch.float32, device=dA.device)
+
+    def hg():
+        st = sgc.sgemm_cube_hgemm(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, Ch.data_ptr(), N,
+                                  stream.cuda_stream)
+        if st:
+            raise sgc.SgemmCubeError(st, "sgemm_cube_hgemm")
+
+    t = _timed_ms(hg, stream, 10)
+    out["hgemm_call"] = {"ms": t, "tflops": flops / (t * 1e-3) / 1e12,
+                         "what": "sgemm_cube_hgemm: FP32 in, fl16(A) fl16(B) on MFMA, FP32 out"}
+    Cf = torch.empty((M, N), dtype=torch.float32, device=dA.device)
+    t = _timed_ms(lambda: torch.matmul(dA, dB, out=Cf), stream, 10)
+    out["vendor_fp32_gemm"] = {"ms": t, "tflops": flops / (t * 1e-3) / 1e12,
+                               "what": "torch.matmul on FP32 tensors"}
+    if with_errors:
+        torch.cuda.synchronize()
+        out["vendor_fp32_gemm"]["errors"] = error_report(Cf.cpu().numpy()[rows], A, B, rows)
+    del Cf
+    hA, hB = dA.half(), dB.half()
+    Ch16 = torch.empty((M, N), dtype=torch.float16, device=dA.device)
+    t = _timed_ms(lambda: torch.matmul(hA, hB, out=Ch16), stream, 10)
+    out["vendor_fp16_gemm"] = {"ms": t, "tflops": flops / (t * 1e-3) / 1e12,
+                               "what": "torch.matmul on FP16 tensors (conversion not timed)"}
+    del hA, hB, Ch16, Ch
+    return out
+
+
 def error_report(C_rows, A, B, rows):
     """Context errors against an FP64 GEMM on sampled rows (Sec. 6.2 Eq. err
     plus the componentwise forms)."""
@@ -181,6 +238,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-errors", action="store_true")
+    ap.add_argument("--no-context", action="store_true",
+                    help="skip the FP16-baseline and vendor-GEMM reference timings")
     ap.add_argument("--copy-mib", type=int, default=512,
                     help="size of the calibration copy (0 = skip)")
     args = ap.parse_args()
@@ -341,6 +400,11 @@ def main():
         torch.cuda.synchronize()
         extra["errors"]["hgemm_fp16"] = error_report(Ch.cpu().numpy()[rows], A, B, rows)
         extra["max_rel_err"] = extra["errors"][order]["max_rel_err"]
+
+    if not args.no_context:
+        log("context: FP16 baseline and vendor GEMM timings")
+        rows = workloads.sample_rows(M, 8, w.seed + 3)
+        extra["context"] = context_gemms(sgc, dA, dB, A, B, rows, stream, not args.no_errors)
 
     cpu = None
     if not args.no_cpu_baseline:
