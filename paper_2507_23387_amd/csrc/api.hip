@@ -433,6 +433,19 @@ int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t ld
   return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, 1.0f, sgc::kHiOnly, stream);
 }
 
+int sgemm_cube_mfma_loop(int64_t workgroups, int64_t iters, const uint16_t* operands,
+                         size_t operand_bytes, float* out, size_t out_bytes, hipStream_t stream) {
+  if (workgroups < 1 || workgroups > 65536 || iters < 1 || iters > 65536 ||
+      workgroups * iters > (int64_t{1} << 26))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!operands || !out || operand_bytes < 65536 ||
+      out_bytes < static_cast<size_t>(workgroups) * 256 * sizeof(float))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  return sgc::launch_mfma_loop(workgroups, iters, operands, out, stream) == hipSuccess
+             ? SGEMM_CUBE_OK
+             : SGEMM_CUBE_ERR_HIP;
+}
+
 const char* sgemm_cube_status_string(int status) {
   switch (status) {
     case SGEMM_CUBE_OK: return "SGEMM_CUBE_OK";
