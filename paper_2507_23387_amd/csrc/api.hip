@@ -7,6 +7,7 @@
 #include <cstring>
 #include <mutex>
 
+#include "ceiling.h"
 #include "internal.h"
 #include "sgemm_cube.h"
 

@@ -11,6 +11,7 @@
 // dependent MFMAs on one accumulator are 64 apart.  Thread t of every
 // workgroup reads fragments 16 t .. 16 t + 15 of the 4096-fragment operand
 // block and writes the sum of its 256 accumulator values to out[256 b + t].
+#include "ceiling.h"
 #include "gemm_common.h"
 
 namespace sgc {

@@ -166,12 +166,6 @@ hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
 hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                                 float scale, hipStream_t stream);
 
-// Enqueue the register-only MFMA loop (ceiling.hip) on `workgroups`
-// workgroups of 256 threads, `iters` iterations of 64 MFMAs per wave; the
-// 64 KiB at `operands` are read, out receives workgroups x 256 floats.
-hipError_t launch_mfma_loop(int64_t workgroups, int64_t iters, const uint16_t* operands,
-                            float* out, hipStream_t stream);
-
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);
