@@ -365,12 +365,15 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // A slots (A_hi, A_lo of 256 rows x 32 k: 32 KiB) and two B slots (B_hi,
 // B_lo of 128 columns: 16 KiB).  A wave keeps its 64 rows of A for the step
 // in registers and streams B one 16-column block at a time, one block ahead;
-// during step kt it reads the A fragments of step kt+1 into a second set (one
-// or two per block, blocks 0-6) and issues 12 DMAs (B stage kt+1, A stage
-// kt+2; three in each of blocks 0-3, so that they land before the barrier:
-// spread two per block over blocks 0-5 they left the block-fold orders 5-6 %
-// slower).  One barrier per step, before the last block, publishes B stage
-// kt+1 and A stage kt+2 and retires B stage kt and A stage kt+1.
+// during step kt it issues 12 DMAs (B stage kt+1, then A stage kt+2; three in
+// each of blocks 0-3: spread two per block over blocks 0-5 they left the
+// block-fold orders 5-6 % slower) and reads the A fragments of step kt+1 into
+// a second set (one or two per block, blocks 2-6).  Two barriers per step:
+// before block 2, A stage kt+1 (copied during step kt-1) has landed; before
+// block 7, B stage kt+1 has, and B stage kt is retired.  The A copies so get
+// a step and two blocks to land, not five blocks: with planes larger than the
+// last-level cache (K = 16384) the single barrier that waited for all copies
+// of the step left termwise 18 % slower.
 constexpr int kTwM = 256;
 constexpr int kTwN = 128;
 constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
@@ -497,17 +500,25 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
 
   // Column block j issues its 12 MFMAs: termwise HH(., j), XA(., j),
   // XB(., j); elementwise HH into acc, XA_g, XB_g; cross-first HH_g, XA_g,
-  // then XB_g chained onto XA_g.  After MFMA m of a block: m = 1, 7 read the
-  // next A fragments, m = 2, 6, 10 of blocks 0-3 issue the DMAs, and in the
-  // block-fold orders MFMAs 3-11 are each followed by 1-2 of the 16 folds of
-  // the previous column block.
+  // then XB_g chained onto XA_g.  After MFMA m of a block: m = 1, 7 of blocks
+  // 2-6 read the next A fragments, m = 2, 6, 10 of blocks 0-3 issue the DMAs
+  // (the 4 of B first), and in the block-fold orders MFMAs 3-11 are each
+  // followed by 1-2 of the 16 folds of the previous column block.  DMAs
+  // complete in issue order, so a vmcnt wait retires all but the newest.
+  constexpr int kDmaPerBlock = 3, kBDmas = 4, kADmas = 8;
+  static_assert(kBDmas + kADmas == 4 * kDmaPerBlock && kBDmas <= 2 * kDmaPerBlock,
+                "the B DMAs of a step are issued in blocks 0-1, before its A DMAs");
   auto step = [&](int kt, half8 (&ah)[kRows], half8 (&al)[kRows], half8 (&nh)[kRows],
                   half8 (&nl)[kRows]) {
     static_for<kCols>([&](auto J) {
       constexpr int j = decltype(J)::value, c = j & 1;
       constexpr int jp = (j + kCols - 1) % kCols;  // the block folded now
+      if constexpr (j == 2) {
+        wait_vmcnt<2 * kDmaPerBlock>();  // all but blocks 0-1's DMAs: A stage kt+1 is in
+        lds_barrier();
+      }
       if constexpr (j == kCols - 1) {
-        wait_vmcnt<0>();
+        wait_vmcnt<kADmas>();  // all but this step's A DMAs: B stage kt+1 is in
         lds_barrier();
         bh[c ^ 1] = rd_b(kt + 1, 0, 0);
         bl[c ^ 1] = rd_b(kt + 1, 1, 0);
@@ -516,8 +527,10 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
         bl[c ^ 1] = rd_b(kt, 1, j + 1);
       }
       SCHED_FENCE();
-      // A fragments rb .. re-1 of the 8 (A_hi blocks 0-3, then A_lo).
-      constexpr int rb = (8 * j + 6) / 7, re = (8 * (j + 1) + 6) / 7;
+      // A fragments rb .. re-1 of the 8 (A_hi blocks 0-3, then A_lo), read in
+      // blocks 2-6.
+      constexpr int rb = j < 2 ? 0 : (8 * (j - 2) + 4) / 5;
+      constexpr int re = j < 2 ? 0 : (8 * (j - 1) + 4) / 5;
       static_for<3 * kRows>([&](auto Mc) {
         constexpr int m = decltype(Mc)::value, g = m / kRows, i = m % kRows;
         if constexpr (V == kTermwise) {
@@ -555,7 +568,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
               nl[r - kRows] = rd_a(kt + 1, 1, r - kRows);
           }
         }
-        if constexpr (j < 4 && m % 4 == 2) dma(kt, 3 * j + m / 4);
+        if constexpr (j < 4 && m % 4 == 2) dma(kt, kDmaPerBlock * j + m / 4);
         SCHED_FENCE();
       });
     });
