@@ -21,10 +21,9 @@ enum Variant : int { kElementwise = 0, kTermwise = 1, kHiOnly = 2, kCrossFirst =
 // DMA into LDS reads whole cache lines.  Inside a tile, row r holds its 16
 // values as two 16-byte chunks; chunk c is stored at position c ^ tile_swizzle(r)
 // with tile_swizzle(r) = bit 4 of r.  With that swap the 16-byte fragment reads
-// of both GEMM kernels from LDS are free of bank conflicts on gfx950 (measured
-// with the LDS bank-conflict counter): 16 rows x 4 chunks of a 32-wide k-step
-// for v_mfma_f32_16x16x32_f16, 32 rows x 2 chunks of a 16-wide k-step for
-// v_mfma_f32_32x32x16_f16.  The GEMM copies tiles into LDS verbatim.
+// of the GEMM kernels from LDS (16 rows x 4 chunks of a 32-wide k-step for
+// v_mfma_f32_16x16x32_f16) are free of bank conflicts on gfx950 (measured with
+// the LDS bank-conflict counter).  The GEMM copies tiles into LDS verbatim.
 constexpr int kPanel = 128;                     // rows per panel
 constexpr int kSlice = 16;                      // k per tile
 constexpr int kTileHalves = kPanel * kSlice;    // 2048 halves = 4 KiB

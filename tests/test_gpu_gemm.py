@@ -29,9 +29,8 @@ SHAPES = [
 
 
 def _kb(order="elementwise"):
-    """The oracle's block size matching the GPU's (the same for every order:
-    one 16 x 16 x 32 MFMA k-step on the scaled elementwise kernel, two
-    32 x 32 x 16 k-steps on the 256 x 128 kernel)."""
+    """The oracle's block size matching the GPU's: one 32-wide k-step of
+    v_mfma_f32_16x16x32_f16, the same in every order and kernel."""
     from paper_2507_23387_amd import binding
 
     return binding.sgemm_cube_block_k()
