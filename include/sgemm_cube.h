@@ -177,8 +177,8 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
  * the three-product GEMM (Eq. recover_eqn, Sec. 4.5), reading A as FP32.
  * Gives the same bits as sgemm_cube_ws(...), i.e. as prepare(A = NULL, B)
  * followed by prepare(A, B = NULL) and compute.
- * For the elementwise order, when A is 16-byte aligned and lda and K are
- * multiples of 4, the split of A happens inside the GEMM kernel (in
+ * For the elementwise order, when scale <= 2^15, A is 16-byte aligned and
+ * lda and K are multiples of 4, the split of A happens inside the GEMM kernel (in
  * registers, with the same arithmetic as the split kernels, so the result is
  * the same) and the A planes are not written unless the scaled kernel cannot
  * run (some |fl16(B)| * scale > 65504); no pass over A goes through HBM
@@ -240,27 +240,6 @@ int sgemm_cube_split(int64_t rows, int64_t cols, const float* X, int64_t ldx, ui
 int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                      const float* B, int64_t ldb, float* C, int64_t ldc, hipStream_t stream);
 
-/*
- * Diagnostic, not part of the method: the register-only loop of the matrix
- * instruction the GEMM kernels use (v_mfma_f32_16x16x32_f16), to measure the
- * rate the matrix units sustain on given FP16 operand data under the board's
- * power limit, i.e. the practical ceiling of the GEMM kernels' fraction of
- * the published FP16 peak.  Launches `workgroups` workgroups of 4 waves; each
- * wave keeps 8 A and 8 B fragments in registers and issues 64 * iters MFMAs
- * into 64 accumulators of 16 x 16, no memory traffic inside the loop.  One
- * launch performs workgroups * 4 * iters * 64 * 16384 FLOP.
- *   operands  device pointer to 32768 FP16 values (operand_bytes >= 65536),
- *             read by every workgroup; the data decides the power drawn.
- *   out       device pointer, out_bytes >= workgroups * 256 * 4: out[256 b + t]
- *             = sum of thread t's accumulator values in workgroup b (with
- *             every operand 0.5: exactly 2048 * iters for iters <= 8192).
- *   1 <= workgroups <= 65536, 1 <= iters <= 65536, workgroups * iters <= 2^26.
- * Allocates nothing; returns SGEMM_CUBE_ERR_INVALID_VALUE for arguments out
- * of range or NULL pointers before any device work.
- */
-int sgemm_cube_mfma_loop(int64_t workgroups, int64_t iters, const uint16_t* operands,
-                         size_t operand_bytes, float* out, size_t out_bytes, hipStream_t stream);
-
 /* Static, human-readable name of a status code. */
 const char* sgemm_cube_status_string(int status);
 
@@ -268,11 +247,12 @@ const char* sgemm_cube_status_string(int status);
  * the main path a block is one MFMA k-step: the running accumulator holds
  * scale * acc and each block's three products are summed into it by the
  * matrix unit in the order HH, XA, XB, each sum rounded once together with
- * the accumulator.  When some |fl16(B)| * scale exceeds 65504 (scale * B_hi
- * would overflow FP16) the elementwise order runs unscaled with blocks of
- * the same size instead: HH into the accumulator, XA_g and XB_g summed
- * separately, acc = (acc + XA_g / s) + XB_g / s.  The cross-terms-first order
- * uses the same block size. */
+ * the accumulator.  When scale > 2^15 (scale is then not a finite FP16 value)
+ * or some |fl16(B)| * scale exceeds 65504 (scale * B_hi would overflow FP16)
+ * the elementwise order runs unscaled with blocks of the same size instead:
+ * HH into the accumulator, XA_g and XB_g summed separately,
+ * acc = (acc + XA_g / s) + XB_g / s.  The cross-terms-first order uses the
+ * same block size. */
 int sgemm_cube_block_k(void);
 
 #ifdef __cplusplus

@@ -43,7 +43,7 @@ EXPORTS = (
     "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_a",
     "sgemm_cube_compute_stages",
     "sgemm_cube_workspace_size", "sgemm_cube_split",
-    "sgemm_cube_hgemm", "sgemm_cube_mfma_loop", "sgemm_cube_status_string",
+    "sgemm_cube_hgemm", "sgemm_cube_status_string",
     "sgemm_cube_block_k",
 )
 
@@ -78,7 +78,6 @@ def _load() -> ctypes.CDLL:
         "sgemm_cube_workspace_size": (sz, [i64, i64, i64, i32]),
         "sgemm_cube_split": (i32, [i64, i64, ptr, i64, ptr, ptr, i64, f32, ptr]),
         "sgemm_cube_hgemm": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, ptr]),
-        "sgemm_cube_mfma_loop": (i32, [i64, i64, ptr, sz, ptr, sz, ptr]),
         "sgemm_cube_status_string": (ctypes.c_char_p, [i32]),
         "sgemm_cube_block_k": (i32, []),
     }
@@ -144,12 +143,6 @@ def sgemm_cube_split(rows, cols, X, ldx, hi, lo, ldh, scale, stream) -> int:
 
 def sgemm_cube_hgemm(M, N, K, A, lda, B, ldb, C, ldc, stream) -> int:
     return _lib.sgemm_cube_hgemm(M, N, K, A, lda, B, ldb, C, ldc, stream)
-
-
-def sgemm_cube_mfma_loop(workgroups, iters, operands, operand_bytes, out, out_bytes,
-                         stream) -> int:
-    return _lib.sgemm_cube_mfma_loop(workgroups, iters, operands, operand_bytes, out, out_bytes,
-                                     stream)
 
 
 def sgemm_cube_status_string(status: int) -> str:

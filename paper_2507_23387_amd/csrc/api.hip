@@ -7,7 +7,6 @@
 #include <cstring>
 #include <mutex>
 
-#include "ceiling.h"
 #include "internal.h"
 #include "sgemm_cube.h"
 
@@ -134,10 +133,11 @@ RangeOpts range_opts(unsigned options, bool report, float scale) {
 }
 
 // sgemm_cube_compute_a: the elementwise order splits A inside the GEMM
-// (gemm_fused.hip) when A's rows can be read as 16-byte vectors.
-bool fused_a_ok(const float* A, int64_t lda, int64_t K, int variant) {
-  return variant == kElementwise && reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 &&
-         K % 4 == 0;
+// (gemm_fused.hip) when A's rows can be read as 16-byte vectors and s is a
+// finite FP16 value (the fused kernel keeps the scaled accumulator).
+bool fused_a_ok(const float* A, int64_t lda, int64_t K, int variant, float scale) {
+  return variant == kElementwise && scaled_kernel_ok(scale) &&
+         reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 && K % 4 == 0;
 }
 
 // GEMM from FP32 A and a workspace whose B planes are prepared: the fused
@@ -146,7 +146,7 @@ bool fused_a_ok(const float* A, int64_t lda, int64_t K, int variant) {
 hipError_t compute_from_a(const Planes& p, int64_t M, int64_t N, int64_t K, const float* A,
                           int64_t lda, float* C, int64_t ldc, float scale, int variant,
                           hipStream_t stream) {
-  if (fused_a_ok(A, lda, K, variant)) {
+  if (fused_a_ok(A, lda, K, variant, scale)) {
     const hipError_t e = launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, stream);
     if (e != hipSuccess) return e;
     return launch_gemm_fallback(p, M, N, C, ldc, scale, stream);
@@ -432,19 +432,6 @@ int sgemm_cube_hgemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t ld
   // The hi-only baseline does not read the residual planes; the split still
   // fills them so the whole split pass is shared.
   return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, 1.0f, sgc::kHiOnly, stream);
-}
-
-int sgemm_cube_mfma_loop(int64_t workgroups, int64_t iters, const uint16_t* operands,
-                         size_t operand_bytes, float* out, size_t out_bytes, hipStream_t stream) {
-  if (workgroups < 1 || workgroups > 65536 || iters < 1 || iters > 65536 ||
-      workgroups * iters > (int64_t{1} << 26))
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (!operands || !out || operand_bytes < 65536 ||
-      out_bytes < static_cast<size_t>(workgroups) * 256 * sizeof(float))
-    return SGEMM_CUBE_ERR_INVALID_VALUE;
-  return sgc::launch_mfma_loop(workgroups, iters, operands, out, stream) == hipSuccess
-             ? SGEMM_CUBE_OK
-             : SGEMM_CUBE_ERR_HIP;
 }
 
 const char* sgemm_cube_status_string(int status) {

@@ -17,8 +17,10 @@
 //                    flag set) and the cross-terms-first order (end of
 //                    Sec. 4.5).
 //   gemm_hi_kernel   256 x 256 tiles: HH only, the native-FP16 baseline.
-// Both elementwise kernels are launched; each reads the range flag first and
-// the one that does not apply returns at once.
+// For the elementwise order with s <= 2^15 both elementwise kernels are
+// launched; each reads the range flag first and the one that does not apply
+// returns at once.  For s > 2^15, which is not a finite FP16 value, the host
+// launches the unscaled kernel alone.
 //
 // Data path.  The planes are stored as 4 KiB tiles of 128 rows x 16 k in the
 // order and swizzle the LDS wants (internal.h), so one pipeline stage (one
@@ -77,9 +79,11 @@ __device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off
 //   s*acc <- fl(s*acc + A_lo B_hi)       = s * fl(acc + XA_g / s)
 //   s*acc <- fl(s*acc + A_hi B_lo)       = s * fl(acc + XB_g / s)
 // and C = (s*acc) / s at the end.  s B_hi is formed in registers with
-// v_pk_mul_f16; it is exact because s is a power of two, provided
-// |B_hi| s <= 65504, which the split of B checks (the range flag; when it is
-// set this kernel returns at once and gemm_n128_kernel computes C).  Each
+// v_pk_mul_f16 from s converted to FP16; it is exact because s is a power of
+// two, provided s <= 2^15 (checked on the host, which otherwise never launches
+// this kernel) and |B_hi| s <= 65504, which the split of B checks (the range
+// flag; when it is set this kernel returns at once and gemm_n128_kernel
+// computes C).  Each
 // block term is summed by the MFMA together with the accumulator, with one
 // rounding, instead of being rounded to FP32 on its own first.
 //
@@ -385,7 +389,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
-    float* __restrict__ C, int64_t ldc, int M, int N, float inv_s) {
+    float* __restrict__ C, int64_t ldc, int M, int N, float inv_s, int unscaled_only) {
   static_assert(V == kTermwise || V == kElementwise || V == kCrossFirst, "n128 variants");
   constexpr bool kFold = V != kTermwise;
   constexpr int kRows = 4;                   // 16-row blocks per wave
@@ -394,7 +398,10 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   constexpr int kBPlane = kTwN * kStep;      // one B plane of one step: 8 KiB
   constexpr int kBBase = 2 * kTwASlot;       // the B slots follow the two A slots
   if constexpr (V == kElementwise) {
-    if (range[0] != range[1]) return;  // the scaled 256 x 256 kernel handles this case
+    // Unless the host routed the call here (unscaled_only: s is not a finite
+    // FP16 value), the scaled 256 x 256 kernel handles the case where the
+    // range flag is clear.
+    if (!unscaled_only && range[0] != range[1]) return;
   }
   extern __shared__ __align__(16) uint16_t lds[];
 
@@ -623,7 +630,7 @@ hipError_t launch_hi(const Planes& p, int64_t M, int64_t N, float* C, int64_t ld
 
 template <int V>
 hipError_t launch_n128(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                       hipStream_t stream) {
+                       hipStream_t stream, bool unscaled_only = false) {
   static std::atomic<bool> done[kMaxDevices];
   const hipError_t attr = set_lds(&gemm_n128_kernel<V>, kTwLdsBytes, done);
   if (attr != hipSuccess) return attr;
@@ -632,7 +639,7 @@ hipError_t launch_n128(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
   hipLaunchKernelGGL((gemm_n128_kernel<V>), dim3(tiles_m * tiles_n), dim3(kWideThreads),
                      kTwLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
                      static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
-                     static_cast<int>(N), 1.0f / s);
+                     static_cast<int>(N), 1.0f / s, unscaled_only ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -642,6 +649,8 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
                        float scale, int variant, hipStream_t stream) {
   switch (variant) {
     case kElementwise: {
+      if (!scaled_kernel_ok(scale))
+        return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream, true);
       const hipError_t e = launch_el<true>(p, M, N, C, ldc, scale, stream);
       if (e != hipSuccess) return e;
       return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
@@ -660,6 +669,9 @@ hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C,
 
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, hipStream_t stream) {
+  if (stages < 1 || stages > 2) return hipErrorInvalidValue;
+  if (!scaled_kernel_ok(scale))
+    return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream, true);
   hipError_t e = hipSuccess;
   switch (stages) {
     case 1: e = launch_el<false>(p, M, N, C, ldc, scale, stream); break;

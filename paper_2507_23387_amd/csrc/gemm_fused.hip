@@ -297,6 +297,7 @@ __global__ __launch_bounds__(kFThreads, 1) void gemm_fused_a_kernel(
 hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
                                const float* A, int64_t lda, float* C, int64_t ldc, float scale,
                                hipStream_t stream) {
+  if (!scaled_kernel_ok(scale)) return hipErrorInvalidValue;  // s must be a finite FP16 value
   static std::atomic<bool> done[kMaxDevices];
   const hipError_t attr = set_lds(&gemm_fused_a_kernel, kFLdsBytes, done);
   if (attr != hipSuccess) return attr;

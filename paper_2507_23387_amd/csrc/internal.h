@@ -161,13 +161,21 @@ hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
                                hipStream_t stream);
 
 // The unscaled elementwise kernel alone; it computes C only when the range
-// flag is set (and returns at once otherwise).
+// flag is set (and returns at once otherwise).  Used after the fused kernel,
+// which is only launched when scaled_kernel_ok(scale).
 hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                                 float scale, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);
+
+// The scaled elementwise kernels form s * B_hi in FP16, which needs s itself
+// to be a finite FP16 value: s <= 2^15 (2^16 rounds to +inf).  Larger scales,
+// which the C-ABI accepts up to 2^24, always take the unscaled elementwise
+// kernel; the host decides this before any launch.
+constexpr float kMaxScaledScale = 32768.0f;
+inline bool scaled_kernel_ok(float scale) { return scale <= kMaxScaledScale; }
 
 // The elementwise k-block of the scaled kernel, of the fallback kernel used
 // when the range flag is set and of the cross-terms-first order: one

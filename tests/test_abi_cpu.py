@@ -207,20 +207,3 @@ def test_compute_a_validation(lib):
     assert call(M=-1) == INVALID
     assert call(M=1 << 31) == NOT_SUPPORTED
     assert call(M=0) == 0                          # validation only: a no-op
-
-
-def test_mfma_loop_rejects_bad_arguments(lib):
-    # Every check happens before any device work (no GPU needed).
-    big = 1 << 16
-    cases = [
-        (0, 1, 1, big, 1, 1024),          # no workgroups
-        (1, 0, 1, big, 1, 1024),          # no iterations
-        (65537, 1, 1, big, 1, 65537 * 1024),
-        (1025, 65536, 1, big, 1, 1025 * 1024),  # workgroups * iters > 2^26
-        (1, 1, None, big, 1, 1024),       # NULL operands
-        (1, 1, 1, big - 2, 1, 1024),      # operands shorter than 64 KiB
-        (1, 1, 1, big, None, 1024),       # NULL out
-        (2, 1, 1, big, 1, 2 * 1024 - 4),  # out shorter than workgroups * 256 floats
-    ]
-    for wg, it, ops, ob, out, outb in cases:
-        assert lib.sgemm_cube_mfma_loop(wg, it, ops, ob, out, outb, None) == 1, (wg, it, ob, outb)
