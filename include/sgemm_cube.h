@@ -103,6 +103,32 @@ int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
                   int64_t ldb, float* C, int64_t ldc, float scale, int accum_order, void* ws,
                   size_t ws_bytes, hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory: code recorded under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same computation, arguments, validation and results as sgemm_cube (bit for
+ * bit: the same kernels run), but the workspace is a fixed device array inside
+ * the library, SGEMM_CUBE_NOALLOC_WORKSPACE_BYTES (64 MiB) on every GPU the
+ * library runs on, held until the process ends.  No device memory is
+ * allocated or freed by this call.
+ *   Problems whose workspace (sgemm_cube_workspace_size) exceeds that size ->
+ *   SGEMM_CUBE_ERR_NOT_SUPPORTED before any device work; the workspace is
+ *   256 + 4 * Kp * (Mp + Np) bytes with Mp, Np = M, N rounded up to 256 and
+ *   Kp = K rounded up to 64, so e.g. M = N = K = 2048 fits.
+ *   All calls on one GPU share its array: calls that overlap in time on one
+ *   GPU (different streams, or different host threads without ordering) race
+ *   and give undefined results; calls ordered on one stream are safe.  The
+ *   array's contents carry over between calls and are never read before each
+ *   call rewrites them.
+ * The first call on each device looks up the array's device address
+ * (hipGetSymbolAddress) with that device current; a failure there ->
+ * SGEMM_CUBE_ERR_HIP.
+ */
+#define SGEMM_CUBE_NOALLOC_WORKSPACE_BYTES ((size_t)64 << 20)
+int sgemm_cube_noalloc(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                       const float* B, int64_t ldb, float* C, int64_t ldc, float scale,
+                       int accum_order, hipStream_t stream);
+
 /* Options of sgemm_cube_ex (bit mask). */
 enum { SGEMM_CUBE_OPT_PRESCALE = 1 };
 

@@ -29,6 +29,7 @@ _EXPORTS = (
     "sgemm_cube_ex",
     "sgemm_cube_ex_workspace_size",
     "sgemm_cube_hgemm",
+    "sgemm_cube_noalloc",
     "sgemm_cube_prepare",
     "sgemm_cube_split",
     "sgemm_cube_status_string",

@@ -39,7 +39,7 @@ STATUS_NAMES = {
 
 # Every symbol include/sgemm_cube.h declares.
 EXPORTS = (
-    "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_ex", "sgemm_cube_ex_workspace_size",
+    "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_noalloc", "sgemm_cube_ex", "sgemm_cube_ex_workspace_size",
     "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_a",
     "sgemm_cube_compute_stages",
     "sgemm_cube_workspace_size", "sgemm_cube_split",
@@ -66,6 +66,8 @@ def _load() -> ctypes.CDLL:
         "sgemm_cube": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32, ptr]),
         "sgemm_cube_ws": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32, ptr, sz,
                                 ptr]),
+        "sgemm_cube_noalloc": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32,
+                                     ptr]),
         "sgemm_cube_ex": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, f32, i32, u32, ptr,
                                 sz, ptr, ptr]),
         "sgemm_cube_ex_workspace_size": (sz, [i64, i64, i64, i32, u32]),
@@ -101,6 +103,13 @@ def sgemm_cube_ws(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, ws, ws_by
                   stream) -> int:
     return _lib.sgemm_cube_ws(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, ws,
                               ws_bytes, stream)
+
+
+def sgemm_cube_noalloc(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, stream) -> int:
+    return _lib.sgemm_cube_noalloc(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, stream)
+
+
+NOALLOC_WORKSPACE_BYTES = 64 << 20  # SGEMM_CUBE_NOALLOC_WORKSPACE_BYTES
 
 
 def sgemm_cube_ex(M, N, K, A, lda, B, ldb, C, ldc, scale, accum_order, options, ws, ws_bytes,

@@ -232,6 +232,34 @@ int run_allocating(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
   return st;
 }
 
+// Workspace of sgemm_cube_noalloc: a fixed device array, one copy per GPU,
+// held for the life of the process.  Host code must not use the array's name
+// as a device address (on the host it names a stand-in object): its device
+// address is looked up once per device with hipGetSymbolAddress, with that
+// device current, and only that address is passed to kernels.  The array's
+// header words are stamped by every split (a fresh stamp per call), so nothing
+// in it has to start at zero; the planes are fully rewritten by the splits of
+// each call, padding included.
+static __device__ __align__(256) unsigned char scratch[SGEMM_CUBE_NOALLOC_WORKSPACE_BYTES];
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return SGEMM_CUBE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+      return SGEMM_CUBE_ERR_HIP;
+    if (reinterpret_cast<uintptr_t>(p) % 256 != 0) return SGEMM_CUBE_ERR_HIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return SGEMM_CUBE_OK;
+}
+
 // sgemm_cube_compute and sgemm_cube_compute_stages; stages == 0 means the
 // library's default pipeline.
 int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale, int accum_order,
@@ -273,6 +301,23 @@ int sgemm_cube(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, con
   if (st != SGEMM_CUBE_OK) return st;
   return sgc::run_allocating(M, N, K, A, lda, B, ldb, C, ldc, scale,
                              sgc::variant_of(accum_order), stream);
+}
+
+int sgemm_cube_noalloc(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                       const float* B, int64_t ldb, float* C, int64_t ldc, float scale,
+                       int accum_order, hipStream_t stream) {
+  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
+  if (st != SGEMM_CUBE_OK) return st;
+  const size_t need = sgc::ws_size(M, N, K);
+  if (need > SGEMM_CUBE_NOALLOC_WORKSPACE_BYTES) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  void* ws = nullptr;
+  if (need > 0) {
+    const int sst = sgc::scratch_address(&ws);
+    if (sst != SGEMM_CUBE_OK) return sst;
+  }
+  return sgc::run(M, N, K, A, lda, B, ldb, C, ldc, scale, sgc::variant_of(accum_order), ws,
+                  stream);
 }
 
 int sgemm_cube_ws(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,

@@ -207,3 +207,20 @@ def test_compute_a_validation(lib):
     assert call(M=-1) == INVALID
     assert call(M=1 << 31) == NOT_SUPPORTED
     assert call(M=0) == 0                          # validation only: a no-op
+
+
+def test_noalloc_validates_before_device_work(lib):
+    """sgemm_cube_noalloc validates like sgemm_cube and refuses problems whose
+    workspace exceeds its fixed 64 MiB array, all before any device call."""
+    def na(M=4, N=4, K=4, A=FAKE, B=FAKE + (1 << 30), C=FAKE + (2 << 30), scale=2048.0, order=0):
+        return lib.sgemm_cube_noalloc(M, N, K, A, max(K, 1), B, max(N, 1), C, max(N, 1), scale,
+                                      order, 0)
+
+    assert lib.NOALLOC_WORKSPACE_BYTES == 64 << 20
+    assert na(M=-1) == INVALID
+    assert na(scale=3.0) == INVALID
+    assert na(order=5) == INVALID
+    assert na(C=FAKE + 8) == INVALID
+    assert na(M=0) == 0 and na(N=0) == 0
+    assert lib.sgemm_cube_workspace_size(4096, 4096, 2049) > lib.NOALLOC_WORKSPACE_BYTES
+    assert na(M=4096, N=4096, K=2049, B=1 << 44, C=1 << 45) == NOT_SUPPORTED
