@@ -66,3 +66,37 @@ def assert_parity(C_gpu: np.ndarray, C_ref: np.ndarray, K: int, absab: np.ndarra
         raise AssertionError(
             f"{what}: {int(bad.sum())} entries exceed 2K u32 |A||B|; worst err={err[idx]:.3e} "
             f"tol={tol[idx]:.3e}")
+
+
+def band_rows(M: int, seed: int, band: int = 256) -> np.ndarray:
+    """One output row in every band of `band` rows (the GEMM's tile height),
+    at an in-band offset that rotates from band to band, plus the first and
+    last rows: every row of tiles of C is sampled."""
+    rng = np.random.default_rng(seed + 104729)
+    start = int(rng.integers(0, band))
+    rows = {0, M - 1}
+    for b in range((M + band - 1) // band):
+        r = b * band + (start + 37 * b) % band
+        rows.add(min(r, M - 1))
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def assert_discriminates(C_gpu: np.ndarray, C_ref: np.ndarray, C_hi: np.ndarray, what: str = "",
+                         frac: float = 0.1):
+    """The GPU result must sit much closer to the oracle than the oracle's
+    hi-only product (the native FP16 GEMM, both correction terms dropped)
+    does: max|C_gpu - C_oracle| <= frac * max|C_oracle - C_hi| and the same
+    for the Frobenius norms.  At long K the componentwise bar 2K u32 |A||B| is
+    looser than the correction terms themselves, so this is what fails when a
+    kernel drops or mis-scales a cross term."""
+    g = np.asarray(C_gpu, dtype=np.float64)
+    r = np.asarray(C_ref, dtype=np.float64)
+    h = np.asarray(C_hi, dtype=np.float64)
+    d, D = np.abs(g - r), np.abs(r - h)
+    assert D.max() > 0, f"{what}: hi-only equals the full result; nothing to discriminate"
+    assert d.max() <= frac * D.max(), (
+        f"{what}: max|gpu - oracle| = {d.max():.3e} > {frac} * max|oracle - hi_only| "
+        f"= {frac * D.max():.3e}")
+    assert np.linalg.norm(d) <= frac * np.linalg.norm(D), (
+        f"{what}: ||gpu - oracle||_F = {np.linalg.norm(d):.3e} > {frac} * "
+        f"||oracle - hi_only||_F = {frac * np.linalg.norm(D):.3e}")
