@@ -110,20 +110,29 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(A, B, w, scale, order, target_s: float):
+# Threads the CPU oracle may use: the host's available cores, capped at the
+# CPU share one GPU gets on the benchmark machines.
+CPU_THREAD_CAP = 16
+
+
+def cpu_baseline(A, B, w, scale, order, target_s: float, kb: int):
     """Time the oracle (as it stands) on a bounded sample of output rows.
 
     Two calibration calls (T and 2T rows, T = threads) separate the per-call
     overhead (the oracle splits and widens all of B on every call) from the
-    per-row cost; the sample is then sized to take about target_s."""
+    per-row cost; the sample is then sized to take about target_s.  Returns
+    the report and the sampled rows with the oracle's values of them (the
+    oracle runs with the GPU's elementwise block size kb, so they also serve
+    as the parity reference)."""
     import oracle
 
-    threads = min(len(os.sched_getaffinity(0)), 16)
+    available = len(os.sched_getaffinity(0))
+    threads = min(available, CPU_THREAD_CAP)
 
     def timed(n):
         rows = workloads.sample_rows(w.M, n, w.seed + n)
         t0 = time.perf_counter()
-        oracle.sgemm_rows(A, B, rows, scale, order, threads=threads)
+        oracle.sgemm_rows(A, B, rows, scale, order, kb=kb, threads=threads)
         return time.perf_counter() - t0
 
     t1 = timed(threads)
@@ -134,20 +143,58 @@ def cpu_baseline(A, B, w, scale, order, target_s: float):
     n = waves * threads
     rows = workloads.sample_rows(w.M, n, w.seed + 2)
     t0 = time.perf_counter()
-    oracle.sgemm_rows(A, B, rows, scale, order, threads=threads)
+    C_rows = oracle.sgemm_rows(A, B, rows, scale, order, kb=kb, threads=threads)
     t = time.perf_counter() - t0
     flops = 2.0 * len(rows) * w.N * w.K
     return {
         "value": flops / t / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
+        "cores_available": available,
+        "cpu_count": os.cpu_count(),
         "cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": f"{len(rows)} of {w.M} output rows of {w.name} ({order}, s=2^"
                   f"{int(np.log2(scale))}), full K={w.K} and N={w.N}; the oracle's split of "
                   f"all of B (about {overhead:.1f} s) included; {t:.1f} s wall",
         "seconds": t,
+    }, rows, C_rows
+
+
+def parity_report(C_gpu_rows, C_oracle_rows, A, B, rows, K):
+    """Verdict of the GPU result against the oracle on sampled rows: the bar
+    |C_gpu - C_oracle|_ij <= 2 K 2^-24 (|A||B|)_ij (equality where
+    (|A||B|)_ij = 0, identical inf/NaN patterns) and its worst ratio."""
+    g = C_gpu_rows.astype(np.float64)
+    o = C_oracle_rows.astype(np.float64)
+    absab = np.abs(A[rows].astype(np.float64)) @ np.abs(B.astype(np.float64))
+    tol = 2.0 * K * 2.0**-24 * absab
+    fin = np.isfinite(o)
+    same_nonfinite = bool(np.array_equal(np.isnan(g), np.isnan(o)) and
+                          np.array_equal(np.isinf(g), np.isinf(o)))
+    err = np.abs(g[fin] - o[fin])
+    t = tol[fin]
+    ok = bool(same_nonfinite and np.all(err <= t))
+    with np.errstate(divide="ignore", invalid="ignore"):
+        ratio = np.where(t > 0, err / t, np.where(err > 0, np.inf, 0.0))
+    return {
+        "verdict": "pass" if ok else "fail",
+        "bar": "|C_gpu - C_oracle| <= 2 K 2^-24 (|A||B|)",
+        "rows": int(len(rows)),
+        "entries": int(g.size),
+        "worst_err_over_tol": float(ratio.max()) if ratio.size else 0.0,
+        "max_abs_err": float(err.max()) if err.size else 0.0,
     }
+
+
+def hi_only_gap(C_gpu_rows, C_oracle_rows, C_hi_rows):
+    """max|C_gpu - C_oracle| / max|C_oracle - C_hi_only| on the same rows: a
+    correct kernel sits far below 1 (the GPU and the oracle differ only in
+    FP32 summation order), one that drops a correction term near or above 1."""
+    g, o, h = (x.astype(np.float64) for x in (C_gpu_rows, C_oracle_rows, C_hi_rows))
+    fin = np.isfinite(o) & np.isfinite(h)
+    gap = np.abs(o - h)[fin].max()
+    return float(np.abs(g - o)[fin].max() / gap) if gap > 0 else None
 
 
 def _timed_ms(fn, stream, reps: int) -> float:
@@ -228,8 +275,9 @@ def main():
     ap.add_argument("--order", default=None, help="elementwise | termwise | elementwise_cross_first")
     ap.add_argument("--scale", type=float, default=None)
     ap.add_argument("--stages", type=int, default=0,
-                    help="elementwise only: LDS stage slots of the 256x256 kernel (1-4; "
-                         "0 = the library's default), through sgemm_cube_compute_stages")
+                    help="elementwise only: 2 = copies overlapped with the MFMAs, 1 = copies "
+                         "issued and waited for at the end of each step (0 = the library's "
+                         "default), through sgemm_cube_compute_stages")
     ap.add_argument("--fused", action="store_true",
                     help="elementwise only: time sgemm_cube_compute_a, whose GEMM kernel splits A "
                          "in registers (the split pass then covers B only)")
@@ -391,15 +439,29 @@ def main():
         "wall_ms_per_step": wall * 1e3 / args.steps,
     }
 
+    import oracle
+
+    kb = sgc.sgemm_cube_block_k()
+    C_gpu = dC.cpu().numpy()  # the result of the last timed step
+
     if not args.no_errors:
-        log("context errors on sampled rows vs FP64")
+        log("context errors on sampled rows vs FP64 (both orders and the FP16 baseline)")
         rows = workloads.sample_rows(M, 8, w.seed + 3)
-        Cn = dC.cpu().numpy()[rows]
-        extra["errors"] = {order: error_report(Cn, A, B, rows)}
+        extra["errors"] = {}
+        for o in ("elementwise", "termwise"):
+            if o == order and not args.prescale:
+                Cn = C_gpu[rows]
+            else:
+                Co_dev = sgc.matmul(dA, dB, scale, o)
+                torch.cuda.synchronize()
+                Cn = Co_dev.cpu().numpy()[rows]
+                del Co_dev
+            extra["errors"][o] = error_report(Cn, A, B, rows)
         Ch = sgc.hgemm(dA, dB)
         torch.cuda.synchronize()
         extra["errors"]["hgemm_fp16"] = error_report(Ch.cpu().numpy()[rows], A, B, rows)
-        extra["max_rel_err"] = extra["errors"][order]["max_rel_err"]
+        del Ch
+        extra["max_rel_err"] = error_report(C_gpu[rows], A, B, rows)["max_rel_err"]
 
     if not args.no_context:
         log("context: FP16 baseline and vendor GEMM timings")
@@ -407,9 +469,31 @@ def main():
         extra["context"] = context_gemms(sgc, dA, dB, A, B, rows, stream, not args.no_errors)
 
     cpu = None
+    oracle_fn = oracle.sgemm_prescaled if args.prescale else oracle.sgemm
     if not args.no_cpu_baseline:
         log(f"cpu baseline (oracle) ~{args.cpu_seconds:.0f} s")
-        cpu = cpu_baseline(A, B, w, scale, order, args.cpu_seconds)
+        if args.prescale:
+            # The oracle's pre-scaled product has no row-sampled form; time the
+            # plain oracle and check parity on band rows below.
+            cpu, prow, C_or = cpu_baseline(A, B, w, scale, order, args.cpu_seconds, kb)
+            prow = workloads.band_rows(M, w.seed)
+            C_or = oracle_fn(A[prow], B, scale, order, kb=kb)
+        else:
+            cpu, prow, C_or = cpu_baseline(A, B, w, scale, order, args.cpu_seconds, kb)
+    else:
+        prow = workloads.band_rows(M, w.seed)
+        C_or = oracle_fn(A[prow], B, scale, order, kb=kb)
+    log(f"parity of the timed result against the oracle on {len(prow)} rows")
+    parity = parity_report(C_gpu[prow], C_or, A, B, prow, K)
+    # The distance to the oracle's hi-only product on one row per 256-row band.
+    brow = workloads.band_rows(M, w.seed + 1)
+    C_band = oracle_fn(A[brow], B, scale, order, kb=kb)
+    C_hi = oracle_fn(A[brow], B, scale, "hi_only", kb=kb)
+    parity["band_rows"] = int(len(brow))
+    parity["band_verdict"] = parity_report(C_gpu[brow], C_band, A, B, brow, K)["verdict"]
+    parity["max_err_over_hi_only_gap"] = hi_only_gap(C_gpu[brow], C_band, C_hi)
+    if parity["band_verdict"] != "pass" or not (parity["max_err_over_hi_only_gap"] or 0) <= 0.1:
+        parity["verdict"] = "fail"
 
     line = {
         "metric": METRIC,
@@ -431,6 +515,7 @@ def main():
                    **({"stages": args.stages} if args.stages else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "parity": parity,
         **extra,
     }
     print(json.dumps(line), flush=True)

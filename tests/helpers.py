@@ -5,6 +5,8 @@ import os
 
 import numpy as np
 
+from workloads import band_rows  # noqa: F401  (re-exported for the tests)
+
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
@@ -66,19 +68,6 @@ def assert_parity(C_gpu: np.ndarray, C_ref: np.ndarray, K: int, absab: np.ndarra
         raise AssertionError(
             f"{what}: {int(bad.sum())} entries exceed 2K u32 |A||B|; worst err={err[idx]:.3e} "
             f"tol={tol[idx]:.3e}")
-
-
-def band_rows(M: int, seed: int, band: int = 256) -> np.ndarray:
-    """One output row in every band of `band` rows (the GEMM's tile height),
-    at an in-band offset that rotates from band to band, plus the first and
-    last rows: every row of tiles of C is sampled."""
-    rng = np.random.default_rng(seed + 104729)
-    start = int(rng.integers(0, band))
-    rows = {0, M - 1}
-    for b in range((M + band - 1) // band):
-        r = b * band + (start + 37 * b) % band
-        rows.add(min(r, M - 1))
-    return np.array(sorted(rows), dtype=np.int64)
 
 
 def assert_discriminates(C_gpu: np.ndarray, C_ref: np.ndarray, C_hi: np.ndarray, what: str = "",

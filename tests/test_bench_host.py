@@ -88,3 +88,35 @@ def test_committed_traffic_file_is_consistent():
     assert e["bytes"] == pytest.approx(e["fetch_bytes"] + e["write_bytes"])
     # Four FP16 planes of 8192 x 8192 read, C written once in FP32.
     assert e["algorithmic_bytes"] == 4 * 8192 * 8192 * 2 + 8192 * 8192 * 4
+
+
+def test_parity_report_passes_within_the_bar_and_fails_outside():
+    import numpy as np
+
+    rng = np.random.default_rng(1)
+    A = rng.uniform(-1, 1, (6, 50)).astype(np.float32)
+    B = rng.uniform(-1, 1, (50, 7)).astype(np.float32)
+    rows = np.array([1, 4])
+    ref = (A[rows].astype(np.float64) @ B.astype(np.float64)).astype(np.float32)
+    absab = np.abs(A[rows].astype(np.float64)) @ np.abs(B.astype(np.float64))
+    tol = 2 * 50 * 2.0**-24 * absab
+    r = bench.parity_report(ref, ref, A, B, rows, 50)
+    assert r["verdict"] == "pass" and r["worst_err_over_tol"] == 0 and r["entries"] == 14
+    near = (ref.astype(np.float64) + 0.5 * tol).astype(np.float32)
+    assert bench.parity_report(near, ref, A, B, rows, 50)["verdict"] == "pass"
+    far = (ref.astype(np.float64) + 3.0 * tol).astype(np.float32)
+    r = bench.parity_report(far, ref, A, B, rows, 50)
+    assert r["verdict"] == "fail" and r["worst_err_over_tol"] > 2
+    nan = ref.copy()
+    nan[0, 0] = np.nan
+    assert bench.parity_report(nan, ref, A, B, rows, 50)["verdict"] == "fail"
+
+
+def test_hi_only_gap():
+    import numpy as np
+
+    o = np.array([[1.0, 2.0]], np.float32)
+    h = np.array([[1.5, 2.0]], np.float32)
+    assert bench.hi_only_gap(o, o, h) == 0.0
+    assert bench.hi_only_gap(o + np.float32(0.25), o, h) == 0.5
+    assert bench.hi_only_gap(o, o, o) is None

@@ -116,3 +116,15 @@ def sample_rows(M: int, count: int, seed: int) -> np.ndarray:
                 break
             rows.add(int(r))
     return np.array(sorted(rows), dtype=np.int64)
+
+
+def band_rows(M: int, seed: int, band: int = 256) -> np.ndarray:
+    """One row index in every band of `band` rows (the GEMM's tile height), at
+    an in-band offset that rotates from band to band, plus the first and last
+    rows: a sample that touches every row of tiles of an M-row output."""
+    rng = np.random.default_rng(seed + 104729)
+    start = int(rng.integers(0, band))
+    rows = {0, M - 1}
+    for b in range((M + band - 1) // band):
+        rows.add(min(b * band + (start + 37 * b) % band, M - 1))
+    return np.array(sorted(rows), dtype=np.int64)
