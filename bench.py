@@ -286,6 +286,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-errors", action="store_true")
+    ap.add_argument("--no-parity", action="store_true",
+                    help="skip the comparison with the oracle (short profiling runs)")
     ap.add_argument("--no-context", action="store_true",
                     help="skip the FP16-baseline and vendor-GEMM reference timings")
     ap.add_argument("--copy-mib", type=int, default=512,
@@ -469,8 +471,13 @@ def main():
         extra["context"] = context_gemms(sgc, dA, dB, A, B, rows, stream, not args.no_errors)
 
     cpu = None
+    parity = None
     oracle_fn = oracle.sgemm_prescaled if args.prescale else oracle.sgemm
-    if not args.no_cpu_baseline:
+    if args.no_parity:
+        if not args.no_cpu_baseline:
+            log(f"cpu baseline (oracle) ~{args.cpu_seconds:.0f} s")
+            cpu = cpu_baseline(A, B, w, scale, order, args.cpu_seconds, kb)[0]
+    elif not args.no_cpu_baseline:
         log(f"cpu baseline (oracle) ~{args.cpu_seconds:.0f} s")
         if args.prescale:
             # The oracle's pre-scaled product has no row-sampled form; time the
@@ -483,17 +490,19 @@ def main():
     else:
         prow = workloads.band_rows(M, w.seed)
         C_or = oracle_fn(A[prow], B, scale, order, kb=kb)
-    log(f"parity of the timed result against the oracle on {len(prow)} rows")
-    parity = parity_report(C_gpu[prow], C_or, A, B, prow, K)
-    # The distance to the oracle's hi-only product on one row per 256-row band.
-    brow = workloads.band_rows(M, w.seed + 1)
-    C_band = oracle_fn(A[brow], B, scale, order, kb=kb)
-    C_hi = oracle_fn(A[brow], B, scale, "hi_only", kb=kb)
-    parity["band_rows"] = int(len(brow))
-    parity["band_verdict"] = parity_report(C_gpu[brow], C_band, A, B, brow, K)["verdict"]
-    parity["max_err_over_hi_only_gap"] = hi_only_gap(C_gpu[brow], C_band, C_hi)
-    if parity["band_verdict"] != "pass" or not (parity["max_err_over_hi_only_gap"] or 0) <= 0.1:
-        parity["verdict"] = "fail"
+    if not args.no_parity:
+        log(f"parity of the timed result against the oracle on {len(prow)} rows")
+        parity = parity_report(C_gpu[prow], C_or, A, B, prow, K)
+        # The distance to the oracle's hi-only product on one row per 256-row band.
+        brow = workloads.band_rows(M, w.seed + 1)
+        C_band = oracle_fn(A[brow], B, scale, order, kb=kb)
+        C_hi = oracle_fn(A[brow], B, scale, "hi_only", kb=kb)
+        parity["band_rows"] = int(len(brow))
+        parity["band_verdict"] = parity_report(C_gpu[brow], C_band, A, B, brow, K)["verdict"]
+        parity["max_err_over_hi_only_gap"] = hi_only_gap(C_gpu[brow], C_band, C_hi)
+        if (parity["band_verdict"] != "pass" or
+                not (parity["max_err_over_hi_only_gap"] or 0) <= 0.1):
+            parity["verdict"] = "fail"
 
     line = {
         "metric": METRIC,

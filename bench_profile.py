@@ -93,8 +93,10 @@ def traffic(fetch_dir, write_dir, workload, order, copy_mib):
     fetch = counters(fetch_dir, "FETCH_SIZE")
     write = counters(write_dir, "WRITE_SIZE")
     copy_kib = copy_mib * 1024.0
-    f_copy = _find(fetch, "copyBuffer")[-1]
-    w_copy = _find(write, "copyBuffer")[-1]
+    # The calibration copy is the largest device copy of the run (the other
+    # copies are small transfers torch makes around it).
+    f_copy = max(_find(fetch, "copyBuffer"))
+    w_copy = max(_find(write, "copyBuffer"))
     f_scale = copy_kib / f_copy
     w_scale = copy_kib / w_copy
     kname = bench.GEMM_KERNELS[order].split("<")[0]
