@@ -41,9 +41,16 @@ METRIC = "FP32-equiv TFLOP/s (2MNK/t) and % of 3-GEMM FP16 MFMA peak; max rel er
 FP16_PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12
 THREE_GEMM_PEAK_TFLOPS = FP16_PEAK_TFLOPS / 3
 HBM_PEAK_GBS = 8000.0
-# The MFMA kernel that runs for each order (the elementwise call also launches
-# the 256 x 128 fallback kernel, which reads the range flag and returns at once).
-GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true>", "termwise": "gemm_n128_kernel<1>",
+# The MFMA kernel that runs for each order: for the elementwise order the
+# 256 x 256 kernel that splits A in registers (where the library chooses it:
+# sgemm_cube_splits_a_in_gemm) or the one that reads the A planes (elsewhere,
+# and with --unfused); either call also launches
+# the unscaled 256 x 128 kernel, which reads the range flag and returns at once
+# unless some |B_hi| s exceeds 65504, in which case it does the work.
+GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true, true>",
+                "elementwise_unfused": "gemm_el_kernel<true, false>",
+                "elementwise_unscaled": "gemm_n128_kernel<0>",
+                "termwise": "gemm_n128_kernel<1>",
                 "elementwise_cross_first": "gemm_n128_kernel<3>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
@@ -81,8 +88,8 @@ def kernel_source_hash() -> str:
     built from: ties a committed HBM-traffic measurement to the kernel it was
     taken on."""
     h = hashlib.sha256()
-    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/gemm_fused.hip",
-                "paper_2507_23387_amd/csrc/gemm_common.h", "paper_2507_23387_amd/csrc/internal.h"):
+    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/gemm_common.h",
+                "paper_2507_23387_amd/csrc/internal.h"):
         with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
             h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
@@ -278,9 +285,9 @@ def main():
                     help="elementwise only: 2 = copies overlapped with the MFMAs, 1 = copies "
                          "issued and waited for at the end of each step (0 = the library's "
                          "default), through sgemm_cube_compute_stages")
-    ap.add_argument("--fused", action="store_true",
-                    help="elementwise only: time sgemm_cube_compute_a, whose GEMM kernel splits A "
-                         "in registers (the split pass then covers B only)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="elementwise only: split A into the workspace and run the GEMM on the A "
+                         "planes also where sgemm_cube would split A inside the GEMM kernel")
     ap.add_argument("--prescale", action="store_true",
                     help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -322,11 +329,14 @@ def main():
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
 
-    # --fused (elementwise only): a step is the split of B (sgemm_cube_prepare
-    # with A = NULL) and sgemm_cube_compute_a, whose kernel splits A in
-    # registers; by default a step is the split of both operands and the GEMM
-    # on the tiled planes, which is what sgemm_cube_ws enqueues.
-    fused = args.fused and order == "elementwise" and not args.stages
+    # A step enqueues what sgemm_cube_ws enqueues.  Where the library splits
+    # A inside the GEMM kernel (sgemm_cube_splits_a_in_gemm) that is the split
+    # of B (sgemm_cube_prepare with A = NULL) and sgemm_cube_compute_a; else,
+    # and with --unfused or --stages, the split of both operands
+    # (sgemm_cube_prepare) and the GEMM on the tiled planes.
+    fused = (not args.unfused and not args.stages and not args.prescale and
+             sgc.binding.sgemm_cube_splits_a_in_gemm(M, N, K, dA.data_ptr(), K, scale,
+                                                     order_code) == 1)
 
     def prepare():
         st = sgc.sgemm_cube_prepare(M, N, K, None if fused else dA.data_ptr(), K, dB.data_ptr(),
@@ -414,10 +424,19 @@ def main():
         del src, dst
 
     gemm_tflops = 3 * flops / (gemm_ms * 1e-3) / 1e12
-    traffic = traffic_entry(w.name, order)
+    kernel_key = order
+    if order == "elementwise":
+        # The range flag: the workspace's first two words are equal after a
+        # split of B that found |B_hi| s > 65504 (s > 2^15 routes there too).
+        hdr = ws[:8].view(torch.int32).cpu()
+        if bool(hdr[0] == hdr[1]) or scale > 32768.0:
+            kernel_key = "elementwise_unscaled"
+        elif not fused:
+            kernel_key = "elementwise_unfused"
+    traffic = traffic_entry(w.name, kernel_key)
     roofline = {
         "bound": "mfma",
-        "kernel": "gemm_fused_a_kernel" if fused else GEMM_KERNELS[order],
+        "kernel": GEMM_KERNELS[kernel_key],
         "achieved": gemm_tflops,
         "peak": FP16_PEAK_TFLOPS,
         "unit": "TFLOP/s",
@@ -520,7 +539,7 @@ def main():
         "config": {"workload": w.name, "M": M, "N": N, "K": K, "seed": w.seed,
                    "distribution": w.dist, "scale": scale, "order": order,
                    **({"prescale": True} if args.prescale else {}),
-                   **({"fused_split_a": True} if fused else {}),
+                   "split_of_a": "in the GEMM kernel" if fused else "separate pass",
                    **({"stages": args.stages} if args.stages else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,

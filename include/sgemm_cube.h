@@ -203,16 +203,13 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
  * the three-product GEMM (Eq. recover_eqn, Sec. 4.5), reading A as FP32.
  * Gives the same bits as sgemm_cube_ws(...), i.e. as prepare(A = NULL, B)
  * followed by prepare(A, B = NULL) and compute.
- * For the elementwise order, when scale <= 2^15, A is 16-byte aligned and
- * lda and K are multiples of 4, the split of A happens inside the GEMM kernel (in
- * registers, with the same arithmetic as the split kernels, so the result is
- * the same) and the A planes are not written unless the scaled kernel cannot
- * run (some |fl16(B)| * scale > 65504); no pass over A goes through HBM
- * besides the GEMM's own reads.  Otherwise A is split into the workspace
- * first.  (On MI355X the fused kernel is slower than the split pass plus the
- * GEMM on the tiled planes, which sgemm_cube and sgemm_cube_ws use: its reads
- * of row-major FP32 A, 128 bytes from each of 256 rows per k-step, cost more
- * than the split pass saves.)
+ * Where sgemm_cube_splits_a_in_gemm(M, N, K, A, lda, scale, accum_order)
+ * returns 1, the split of A happens inside the GEMM kernel (in registers, with
+ * the same arithmetic as the split kernels, so the result is the same) and the
+ * A planes are not written unless the scaled kernel cannot run (some
+ * |fl16(B)| * scale > 65504); no pass over A goes through HBM besides the
+ * GEMM's own reads.  Otherwise A is split into the workspace first.
+ * sgemm_cube, sgemm_cube_ws and sgemm_cube_noalloc follow the same rule.
  * M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes and the errors
  * follow sgemm_cube_ws; C must not overlap A or the workspace.  Must use the
  * same M, N, K and scale as the prepare of B (the library cannot check this).
@@ -221,6 +218,20 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
 int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                          float* C, int64_t ldc, float scale, int accum_order, void* ws,
                          size_t ws_bytes, hipStream_t stream);
+
+/*
+ * 1 when sgemm_cube, sgemm_cube_ws, sgemm_cube_noalloc and
+ * sgemm_cube_compute_a with these arguments split A inside the GEMM kernel
+ * instead of in a pass of its own, else 0 (also for arguments those calls
+ * reject).  The in-kernel split repeats the split of each A tile for every
+ * tile column of C, so it is chosen only where that costs less than the
+ * pass over A: the elementwise order, N <= 4096, scale <= 2^15, A 16-byte
+ * aligned, lda a multiple of 4 and below 2^22, and K a multiple of 64.
+ * Enqueues nothing and reads no device memory (A is only looked at as an
+ * address).  Both choices give the same bits.
+ */
+int sgemm_cube_splits_a_in_gemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                                float scale, int accum_order);
 
 /*
  * Measurement hook for the pipeline ablation (Sec. 5.4 measures double

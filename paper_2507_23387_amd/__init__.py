@@ -32,6 +32,7 @@ _EXPORTS = (
     "sgemm_cube_noalloc",
     "sgemm_cube_prepare",
     "sgemm_cube_split",
+    "sgemm_cube_splits_a_in_gemm",
     "sgemm_cube_status_string",
     "sgemm_cube_workspace_size",
     "sgemm_cube_ws",

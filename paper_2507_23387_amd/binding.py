@@ -41,7 +41,7 @@ STATUS_NAMES = {
 EXPORTS = (
     "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_noalloc", "sgemm_cube_ex", "sgemm_cube_ex_workspace_size",
     "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_a",
-    "sgemm_cube_compute_stages",
+    "sgemm_cube_splits_a_in_gemm", "sgemm_cube_compute_stages",
     "sgemm_cube_workspace_size", "sgemm_cube_split",
     "sgemm_cube_hgemm", "sgemm_cube_status_string",
     "sgemm_cube_block_k",
@@ -75,6 +75,7 @@ def _load() -> ctypes.CDLL:
         "sgemm_cube_compute": (i32, [i64, i64, i64, ptr, i64, f32, i32, ptr, sz, ptr]),
         "sgemm_cube_compute_a": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, i32, ptr, sz,
                                        ptr]),
+        "sgemm_cube_splits_a_in_gemm": (i32, [i64, i64, i64, ptr, i64, f32, i32]),
         "sgemm_cube_compute_stages": (i32, [i64, i64, i64, ptr, i64, f32, i32, i32, ptr, sz,
                                             ptr]),
         "sgemm_cube_workspace_size": (sz, [i64, i64, i64, i32]),
@@ -134,6 +135,10 @@ def sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_byt
                          stream) -> int:
     return _lib.sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes,
                                      stream)
+
+
+def sgemm_cube_splits_a_in_gemm(M, N, K, A, lda, scale, accum_order) -> int:
+    return _lib.sgemm_cube_splits_a_in_gemm(M, N, K, A, lda, scale, accum_order)
 
 
 def sgemm_cube_compute_stages(M, N, K, C, ldc, scale, accum_order, stages, ws, ws_bytes,

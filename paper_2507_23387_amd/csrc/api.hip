@@ -132,25 +132,27 @@ RangeOpts range_opts(unsigned options, bool report, float scale) {
   return o;
 }
 
-// sgemm_cube_compute_a: the elementwise order splits A inside the GEMM
-// (gemm_fused.hip) when A's rows can be read as 16-byte vectors and s is a
-// finite FP16 value (the fused kernel keeps the scaled accumulator).
-bool fused_a_ok(const float* A, int64_t lda, int64_t K, int variant, float scale) {
-  return variant == kElementwise && scaled_kernel_ok(scale) &&
-         reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 && K % 4 == 0;
+// The in-kernel split of A redoes the split of an A tile once per tile
+// column of C, on the vector ALU between the matrix instructions, while the
+// split pass costs one read of A and one write of its planes through HBM.
+// Measured on MI355X with the elementwise order: the in-kernel split is 13%
+// faster at M x N x K = 16384 x 1024 x 8192, 1% faster at 4096^3 and 4%
+// slower at 8192^3, so it is used up to N = 4096.
+constexpr int64_t kFusedSplitMaxN = 4096;
+
+bool splits_a_in_gemm(int64_t N, const float* A, int64_t lda, int64_t K, float scale,
+                      int variant) {
+  return variant == kElementwise && N <= kFusedSplitMaxN && fused_split_ok(A, lda, K, scale);
 }
 
-// GEMM from FP32 A and a workspace whose B planes are prepared: the fused
-// elementwise kernel when it applies, else the split of A and the GEMM on the
-// planes.
+// GEMM from FP32 A and a workspace whose B planes are prepared: the 256 x 256
+// kernel splits A in registers when splits_a_in_gemm says so, else A is split
+// into the workspace first and the GEMM runs on the planes.
 hipError_t compute_from_a(const Planes& p, int64_t M, int64_t N, int64_t K, const float* A,
                           int64_t lda, float* C, int64_t ldc, float scale, int variant,
                           hipStream_t stream) {
-  if (fused_a_ok(A, lda, K, variant, scale)) {
-    const hipError_t e = launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, stream);
-    if (e != hipSuccess) return e;
-    return launch_gemm_fallback(p, M, N, C, ldc, scale, stream);
-  }
+  if (splits_a_in_gemm(N, A, lda, K, scale, variant))
+    return launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, stream);
   const hipError_t e = launch_split_a(p, M, K, A, lda, scale, RangeOpts{}, next_stamp(), stream);
   if (e != hipSuccess) return e;
   return launch_gemm(p, M, N, C, ldc, scale, variant, stream);
@@ -169,6 +171,14 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
     return SGEMM_CUBE_OK;
   }
   const Planes p = plan_planes(M, N, K, ws, opt.prescale);
+  if (!opt.prescale && !opt.report && splits_a_in_gemm(N, A, lda, K, scale, variant)) {
+    // B is split into the workspace, A inside the GEMM kernel.
+    if (launch_split_b(p, K, N, B, ldb, scale, opt, next_stamp(), stream) != hipSuccess)
+      return SGEMM_CUBE_ERR_HIP;
+    return compute_from_a(p, M, N, K, A, lda, C, ldc, scale, variant, stream) == hipSuccess
+               ? SGEMM_CUBE_OK
+               : SGEMM_CUBE_ERR_HIP;
+  }
   if (opt.prescale && launch_absmax(p, M, N, K, A, lda, B, ldb, stream) != hipSuccess)
     return SGEMM_CUBE_ERR_HIP;
   if (launch_split_a(p, M, K, A, lda, scale, opt, next_stamp(), stream) != hipSuccess)
@@ -434,6 +444,14 @@ int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_
                              stream) == hipSuccess
              ? SGEMM_CUBE_OK
              : SGEMM_CUBE_ERR_HIP;
+}
+
+int sgemm_cube_splits_a_in_gemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                                float scale, int accum_order) {
+  if (M <= 0 || N <= 0 || K <= 0 || !A || !sgc::valid_scale(scale)) return 0;
+  if (accum_order < SGEMM_CUBE_ELEMENTWISE || accum_order > SGEMM_CUBE_ELEMENTWISE_CROSS_FIRST)
+    return 0;
+  return sgc::splits_a_in_gemm(N, A, lda, K, scale, sgc::variant_of(accum_order)) ? 1 : 0;
 }
 
 int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc,

@@ -70,6 +70,41 @@ __device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off
                (((fc & 1) ^ tile_swizzle(16 * par + fr)) << 3);
 }
 
+// Split of A into the tiled planes, used when the scaled kernel cannot run
+// and the unscaled kernel that follows needs them: the blocking of the split
+// kernel of A (a block of 16 rows x 128 k per workgroup; lane l of wave w
+// splits 8 consecutive k of row 4w + l / 16, so each row is read as one
+// 512-byte piece and each store fills whole 128-byte lines), the blocks taken
+// in turn by the workgroups of the GEMM grid.  A is 16-byte aligned with lda a
+// multiple of 4 here; rows past M and k past K are written as zeros.
+__device__ void split_a_planes(const float* __restrict__ A, int64_t lda, int M, int K, int Mp,
+                               int Kp, uint16_t* __restrict__ a_hi, uint16_t* __restrict__ a_lo,
+                               float s) {
+  const int lane = threadIdx.x & 63;
+  const int kblocks = (Kp + 127) / 128;
+  const int64_t blocks = static_cast<int64_t>(Mp / 16) * kblocks;
+  for (int64_t b = blockIdx.x; b < blocks; b += gridDim.x) {
+    const int64_t m = (b / kblocks) * 16 + (threadIdx.x >> 6) * 4 + (lane >> 4);
+    const int64_t k0 = (b % kblocks) * 128 + (lane & 15) * 8;
+    if (k0 >= Kp) continue;
+    float v[8];
+    if (m < M && k0 + 7 < K) {
+      const float4* src = reinterpret_cast<const float4*>(A + m * lda + k0);
+      const float4 f0 = src[0], f1 = src[1];
+      v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
+      v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? A[m * lda + k0 + e] : 0.0f;
+    }
+    u32x4 hv, lv;
+    split8(v, s, hv, lv);
+    const int64_t idx = tiled_index(m, k0, Kp);
+    store_stream(a_hi + idx, hv);
+    store_stream(a_lo + idx, lv);
+  }
+}
+
 // Scaled elementwise kernel (Eq. elementwise, Sec. 4.5), one 256 x 256 tile
 // of C per workgroup, 4 waves of 128 x 128 (one per SIMD; 64 accumulators of
 // 16 x 16 in the 256 AGPRs).  The contraction is cut into blocks g of one
@@ -103,21 +138,28 @@ __device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off
 // past the end repeat the last stage, so every wait count is a constant.
 // kPrefetch = false (pipeline ablation): the 16 DMAs of a step are issued
 // right before its barrier, so no copy overlaps the MFMAs.
-template <bool kPrefetch>
+template <bool kPrefetch, bool kFusedA>
 __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
-    const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
+    uint16_t* __restrict__ a_hi, uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
-    float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s) {
+    float* __restrict__ C, int64_t ldc, int M, int N, float s, float inv_s,
+    const float* __restrict__ af, int64_t lda, int K) {
+  static_assert(kPrefetch || !kFusedA, "the fused split runs with the overlapped copies only");
   constexpr int kBBase = 2 * kSlotHalves;     // the B slots follow the two A slots
   constexpr int kDmaCols = 4;                 // column blocks that issue the DMAs
   constexpr int kDmaPerCol = 16 / kDmaCols;   // after MFMAs 2, 8, 14, 20 of a block
-  if (range[0] == range[1]) return;  // s B_hi overflows FP16: gemm_n128_kernel runs instead
-  extern __shared__ __align__(16) uint16_t lds[];
-
   int tm, tn;
   if (!tile_of_block(blockIdx.x, tiles_m, tiles_n, tm, tn))
     tile_of<4>(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  if (range[0] == range[1]) {
+    // s B_hi overflows FP16: gemm_n128_kernel runs instead.  Without planes
+    // of A (fused split), this kernel first writes them for it.
+    if constexpr (kFusedA) split_a_planes(af, lda, M, K, tiles_m * kWide, Kp, a_hi, a_lo, s);
+    return;
+  }
+  extern __shared__ __align__(16) uint16_t lds[];
+
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = w >> 1, wn = w & 1;
@@ -141,12 +183,82 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
            lds_base + (base + (t & 1) * kSlotHalves + p * kStepPlaneHalves +
                        (2 * ph + sl) * kTileHalves) * 2);
   };
+  // Fused split: an A slot holds the FP32 rows of the stage, 256 rows x 32 k
+  // (32 KiB).  Row r's eight 16-byte chunks (k 4q .. 4q+3) sit at chunk
+  // positions q ^ g(r) of its 128 bytes, g(r) = (r & 3) << 1 | bit 3 of r.
+  // Measured with the LDS bank-conflict counter on gfx950: the fragment
+  // reads below (16 rows x 4 chunks per instruction) have no bank conflicts
+  // with this swap, while swaps that leave rows 8 apart (1 KiB) on the same
+  // chunk positions conflict (4-12 extra cycles per read).  DMA n (0-31)
+  // fills rows 8n .. 8n+7, wave w issuing n = w + 4d, d = 0-7: lane l copies
+  // chunk (l & 7) ^ g(r) of row r = 8n + (l >> 3), and
+  // g(r) = ((l >> 3) & 3) << 1 | (w & 1) for every d.  Rows past M repeat row
+  // M - 1 (their results are never stored).  K is a multiple of 64 here, so
+  // no copy reads past a row of A.
+  unsigned a_voff[kFusedA ? 8 : 1];
+  const float* a_tile = nullptr;
+  if constexpr (kFusedA) {
+    const int row0 = tm * kWide;
+    const int q = (lane & 7) ^ ((((lane >> 3) & 3) << 1) | (w & 1));
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const int r = min(row0 + 8 * (w + 4 * d) + (lane >> 3), M - 1) - row0;
+      a_voff[d] = static_cast<unsigned>(r * lda * 4 + q * 16);
+    }
+    a_tile = af + static_cast<int64_t>(row0) * lda;
+  }
+  auto dma_af = [&](int t, int d) {
+    const int tc = min(t, ksteps - 1);
+    dma16s(a_tile + static_cast<int64_t>(tc) * kStep, a_voff[d],
+           lds_base + (t & 1) * kSlotHalves * 2 + d * 4096);
+  };
   // The d-th of the 16 DMAs of step kt: B stage kt+1, then A stage kt+2.
   auto dma = [&](int kt, int d) {
     if (d < 8)
       dma_stage(src_b, kBBase, kt + 1, d);
+    else if constexpr (kFusedA)
+      dma_af(kt + 2, d - 8);
     else
       dma_stage(src_a, 0, kt + 2, d - 8);
+  };
+  // Fused split: lane l's A fragment of row block i is row 16 i + l % 16 of
+  // the wave's 128 rows, k 8c .. 8c + 7 (c = l / 16), i.e. chunks 2c and
+  // 2c + 1 of the row; with the swap above (bits 0, 1 and 3 of the row are
+  // those of l), two 16-byte reads.
+  int af_off[2];
+  const int af_swap = ((lane & 3) << 1) | ((lane >> 3) & 1);
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    af_off[h] = ((lane & 15) * 8 + ((2 * (lane >> 4) + h) ^ af_swap)) * 16;
+  auto rd_af = [&](int t, int i, int h) -> floatx4 {
+    const char* base = reinterpret_cast<const char*>(lds) + (t & 1) * kSlotHalves * 2;
+    return *reinterpret_cast<const floatx4*>(base + (128 * wm + 16 * i) * 128 + af_off[h]);
+  };
+  const float s_sgpr = __builtin_bit_cast(
+      float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, s)));
+  // Instruction k (0-19) of the split of one row block's eight values f
+  // (f[0]: k 8c .. 8c+3, f[1]: 8c+4 .. 8c+7) into the A_hi and A_lo
+  // fragments h, l: the four high words first (k 0-3), then for pairs 0-1
+  // and then 2-3 the residuals and the scaled residual words (k 4-11,
+  // 12-19), five instructions per pair.
+  auto split_k = [&](auto Kc, half8& h, half8& l, const floatx4 (&f)[2], float (&r)[2][2]) {
+    constexpr int k = decltype(Kc)::value;
+    constexpr int pair = k < 4 ? k : 2 * ((k - 4) / 8) + ((k - 4) % 8 < 4 ? ((k - 4) % 8) / 2
+                                                                          : ((k - 4) % 8 - 4) / 2);
+    constexpr int op = k < 4 ? 0 : ((k - 4) % 8 < 4 ? 1 + (k - 4) % 2 : 3 + (k - 4) % 2);
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 hv = __builtin_bit_cast(u32x4, h), lv = __builtin_bit_cast(u32x4, l);
+    uint32_t hw = hv[pair], lw = lv[pair];
+    const float a0 = f[pair / 2][2 * (pair % 2)], a1 = f[pair / 2][2 * (pair % 2) + 1];
+    split_op<op>(hw, lw, r[pair % 2], a0, a1, s_sgpr);
+    if constexpr (op == 0) {
+      hv[pair] = hw;
+      h = __builtin_bit_cast(half8, hv);
+    }
+    if constexpr (op >= 3) {
+      lv[pair] = lw;
+      l = __builtin_bit_cast(half8, lv);
+    }
   };
 
   int a_off[2], b_off[2];
@@ -172,19 +284,41 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
     for (int j = 0; j < kWSub; ++j) acc[i][j] = floatx4{};
 
   // Prologue: A stages 0 and 1 and B stage 0; A stage 0 goes to registers.
-  static_for<8>([&](auto n) { dma_stage(src_a, 0, 0, decltype(n)::value); });
-  static_for<8>([&](auto n) { dma_stage(src_a, 0, 1, decltype(n)::value); });
+  if constexpr (kFusedA) {
+    static_for<8>([&](auto n) { dma_af(0, decltype(n)::value); });
+    static_for<8>([&](auto n) { dma_af(1, decltype(n)::value); });
+  } else {
+    static_for<8>([&](auto n) { dma_stage(src_a, 0, 0, decltype(n)::value); });
+    static_for<8>([&](auto n) { dma_stage(src_a, 0, 1, decltype(n)::value); });
+  }
   static_for<8>([&](auto n) { dma_stage(src_b, kBBase, 0, decltype(n)::value); });
   wait_vmcnt<0>();
   lds_barrier();
   // (AH, AL) and (NH, NL): A_hi, A_lo of the current and of the next step.
   // bh, bl, bs: B_hi, B_lo, s B_hi of a column block, double-buffered by the
-  // parity of the block.
+  // parity of the block.  Fused split: F[i & 1] holds the FP32 fragment of
+  // row block i of the next stage from its reads (one column block before
+  // its split) to its split; rr holds the residuals of two pairs.
   half8 AH[kWSub], AL[kWSub], NH[kWSub], NL[kWSub], bh[2], bl[2], bs[2];
+  floatx4 F[2][2];
+  float rr[2][2];
+  if constexpr (kFusedA) {
 #pragma unroll
-  for (int i = 0; i < kWSub; ++i) {
-    AH[i] = rd_a(0, 0, i);
-    AL[i] = rd_a(0, 1, i);
+    for (int i = 0; i < kWSub; ++i) {
+      AH[i] = AL[i] = half8{};
+      F[0][0] = rd_af(0, i, 0);
+      F[0][1] = rd_af(0, i, 1);
+      static_for<20>([&](auto Kc) { split_k(Kc, AH[i], AL[i], F[0], rr); });
+    }
+    // Row block 0 of stage 1, split during step 0.
+    F[0][0] = rd_af(1, 0, 0);
+    F[0][1] = rd_af(1, 0, 1);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kWSub; ++i) {
+      AH[i] = rd_a(0, 0, i);
+      AL[i] = rd_a(0, 1, i);
+    }
   }
   bh[0] = rd_b(0, 0, 0);
   bl[0] = rd_b(0, 1, 0);
@@ -195,7 +329,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
   // accumulator sees the block terms in the order HH, XA, XB, and the three
   // MFMAs of one accumulator are 8 MFMAs apart.  After MFMA m of a block:
   // m = 1, 9, 17 read the next A fragments, m = 2, 8, 14, 20 of blocks 0-3
-  // issue the DMAs, m = 14 forms the next block's s B_hi.
+  // issue the DMAs, m = 12 and 14 form the next block's s B_hi (two halves:
+  // two VALU instructions overlap an MFMA for free, four do not).
   auto step = [&](int kt, half8 (&ah)[kWSub], half8 (&al)[kWSub], half8 (&nh)[kWSub],
                   half8 (&nl)[kWSub]) {
     static_for<kWSub>([&](auto J) {
@@ -222,8 +357,26 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
         else
           mfma16_acc(acc[i][j], ah[i], bl[c]);
         SCHED_FENCE();
-        if constexpr (m == 14) bs[c ^ 1] = pk_scale(bh[c ^ 1], s2);
-        if constexpr (j < kWSub - 1 && m % kWSub == 1) {
+        if constexpr (kFusedA) {
+          // One VALU instruction after every MFMA: s B_hi of the next block
+          // one word at a time after MFMAs 12-15, and the 20 instructions of
+          // the split after MFMAs 0-11 and 16-23.  Column block j reads row
+          // block j + 1 of stage kt+1 (block 7, after its barrier: row block
+          // 0 of stage kt+2) and splits row block j, read one block earlier,
+          // into the next step's fragments; the last instruction for row
+          // block 7 comes 16 MFMAs before the next step's first use of it.
+          if constexpr (m >= 12 && m <= 15) pk_scale_word<m - 12>(bs[c ^ 1], bh[c ^ 1], s2);
+          constexpr int nxt = (j + 1) % kWSub;
+          if constexpr (m == 1) F[nxt & 1][0] = rd_af(j == kWSub - 1 ? kt + 2 : kt + 1, nxt, 0);
+          if constexpr (m == 3) F[nxt & 1][1] = rd_af(j == kWSub - 1 ? kt + 2 : kt + 1, nxt, 1);
+          constexpr int k = m < 12 ? m : m >= 16 ? m - 4 : -1;
+          if constexpr (k >= 0)
+            split_k(std::integral_constant<int, k>{}, nh[j], nl[j], F[j & 1], rr);
+        } else {
+          if constexpr (m == 12) pk_scale_half<0>(bs[c ^ 1], bh[c ^ 1], s2);
+          if constexpr (m == 14) pk_scale_half<1>(bs[c ^ 1], bh[c ^ 1], s2);
+        }
+        if constexpr (!kFusedA && j < kWSub - 1 && m % kWSub == 1) {
           constexpr int r = rb + m / kWSub;
           if constexpr (r < re) {
             if constexpr (r < kWSub)
@@ -490,18 +643,31 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   bl[0] = rd_b(0, 1, 0);
   lds_barrier();  // A slot 0 is refilled (stage 2) during step 0
 
-  // The fold of column block jp (block sums of parity cp) for rows and
-  // elements q = 4 i + e in [q0, q1).
-  auto fold = [&](int jp, int cp, int q0, int q1) {
+  // The fold of column block jp (block sums of parity cp) in two halves, for
+  // rows and elements q = 4 i + e in [q0, q1):
+  //   elementwise   first  acc = fl(acc + XA_g / s)       (acc holds acc + HH_g)
+  //                 second acc = fl(acc + XB_g / s)
+  //   cross-first   first  HH_g <- fl(X_g / s + HH_g)
+  //                 second acc = fl(acc + HH_g)
+  // One v_fma_f32 or v_add_f32 per element and half (1/s is exact).
+  auto fold_first = [&](int jp, int cp, int q0, int q1) {
 #pragma unroll
     for (int q = q0; q < q1; ++q) {
       const int i = q >> 2, e = q & 3;
-      if constexpr (V == kElementwise) {
-        float v = __builtin_fmaf(t1[cp][i][e], inv_s, hh[i][jp][e]);
-        hh[i][jp][e] = __builtin_fmaf(t2[cp][i][e], inv_s, v);
-      } else {
-        hh[i][jp][e] += __builtin_fmaf(t1[cp][i][e], inv_s, t2[cp][i][e]);
-      }
+      if constexpr (V == kElementwise)
+        hh[i][jp][e] = __builtin_fmaf(t1[cp][i][e], inv_s, hh[i][jp][e]);
+      else
+        t2[cp][i][e] = __builtin_fmaf(t1[cp][i][e], inv_s, t2[cp][i][e]);
+    }
+  };
+  auto fold_second = [&](int jp, int cp, int q0, int q1) {
+#pragma unroll
+    for (int q = q0; q < q1; ++q) {
+      const int i = q >> 2, e = q & 3;
+      if constexpr (V == kElementwise)
+        hh[i][jp][e] = __builtin_fmaf(t2[cp][i][e], inv_s, hh[i][jp][e]);
+      else
+        hh[i][jp][e] += t2[cp][i][e];
     }
   };
 
@@ -563,9 +729,34 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
             mfma16_va_acc(t1[c][i], ah[i], bl[c]);
         }
         SCHED_FENCE();
-        // Folds after MFMAs 3-11: every sum read here was written at least 8
-        // MFMAs earlier (XB_g of row i, the last, by MFMA 8 + i of block jp).
-        if constexpr (kFold && m >= 3) fold(jp, c ^ 1, (16 * (m - 3)) / 9, (16 * (m - 2)) / 9);
+        // Folds: at most three VALU operations after any MFMA (up to two
+        // overlap an MFMA for free; each further one costs its issue time).
+        // Every block sum is read at least 8 MFMAs after the MFMA that wrote
+        // it, and before the MFMA of a later block that overwrites it.
+        if constexpr (V == kElementwise) {
+          // Block jp: XA_g of row i written by its MFMA 4 + i, XB_g by 8 + i,
+          // so the first half of row i may run after MFMA m >= i here and
+          // the second after m >= 4 + i.  Both halves of the 16 elements:
+          // 3,3,3,3,2,2 per MFMA over MFMAs 0-5, then 2,2,3,3,3,3 over 6-11.
+          constexpr int f1[7] = {0, 3, 6, 9, 12, 14, 16};
+          constexpr int f2[7] = {0, 2, 4, 7, 10, 13, 16};
+          if constexpr (m < 6) fold_first(jp, c ^ 1, f1[m], f1[m + 1]);
+          else fold_second(jp, c ^ 1, f2[m - 6], f2[m - 5]);
+        } else if constexpr (V == kCrossFirst) {
+          // Block jp: X_g of row i complete after its MFMA 8 + i, HH_g after
+          // MFMA i, so the first half of row i may run after m >= 4 + i.  The
+          // second half of rows 2-3 spills into the next block's MFMAs 0-2:
+          // that block (parity cp) overwrites HH_g of row i with its MFMA i.
+          constexpr int f1[7] = {0, 3, 6, 9, 12, 15, 16};  // after MFMAs 4-9
+          constexpr int f2[6] = {0, 2, 5, 8, 11, 14};      // after MFMAs 9-11, next 0-1
+          if constexpr (m >= 4 && m <= 9) fold_first(jp, c ^ 1, f1[m - 4], f1[m - 3]);
+          if constexpr (m >= 9) fold_second(jp, c ^ 1, f2[m - 9], f2[m - 8]);
+          // The spill of block j - 2 (the same parity as this block).
+          constexpr int jpp = (j + kCols - 2) % kCols;
+          if constexpr (m == 0) fold_second(jpp, c, 8, 11);
+          if constexpr (m == 1) fold_second(jpp, c, 11, 14);
+          if constexpr (m == 2) fold_second(jpp, c, 14, 16);
+        }
         if constexpr (j < kCols - 1 && (m == 1 || m == 7)) {
           constexpr int r = rb + m / 6;
           if constexpr (r < re) {
@@ -586,7 +777,14 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   }
   wait_vmcnt<0>();
   mfma_drain();
-  if constexpr (kFold) fold(kCols - 1, 1, 0, 4 * kRows);
+  if constexpr (V == kElementwise) {
+    fold_first(kCols - 1, 1, 0, 4 * kRows);
+    fold_second(kCols - 1, 1, 0, 4 * kRows);
+  } else if constexpr (V == kCrossFirst) {
+    fold_second(kCols - 2, 0, 8, 4 * kRows);  // the spill of block 6
+    fold_first(kCols - 1, 1, 0, 4 * kRows);
+    fold_second(kCols - 1, 1, 0, 4 * kRows);
+  }
 
   const int col0 = tn * kTwN + (lane & 15);
   const int row0 = tm * kTwM + w * 64 + (lane >> 4) * 4;
@@ -600,18 +798,20 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   });
 }
 
-template <bool kPrefetch>
+template <bool kPrefetch, bool kFusedA>
 hipError_t launch_el(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                     hipStream_t stream) {
+                     hipStream_t stream, const float* A = nullptr, int64_t lda = 0,
+                     int64_t K = 0) {
   static std::atomic<bool> done[kMaxDevices];
-  const hipError_t attr = set_lds(&gemm_el_kernel<kPrefetch>, kElLdsBytes, done);
+  const hipError_t attr = set_lds(&gemm_el_kernel<kPrefetch, kFusedA>, kElLdsBytes, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kWide);
   const int tiles_n = static_cast<int>(p.Np / kWide);
-  hipLaunchKernelGGL((gemm_el_kernel<kPrefetch>), dim3(tiles_m * tiles_n), dim3(kWideThreads),
-                     kElLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
-                     static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
-                     static_cast<int>(N), s, 1.0f / s);
+  hipLaunchKernelGGL((gemm_el_kernel<kPrefetch, kFusedA>), dim3(tiles_m * tiles_n),
+                     dim3(kWideThreads), kElLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo,
+                     p.range, static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc,
+                     static_cast<int>(M), static_cast<int>(N), s, 1.0f / s, A, lda,
+                     static_cast<int>(K));
   return hipGetLastError();
 }
 
@@ -651,7 +851,7 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
     case kElementwise: {
       if (!scaled_kernel_ok(scale))
         return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream, true);
-      const hipError_t e = launch_el<true>(p, M, N, C, ldc, scale, stream);
+      const hipError_t e = launch_el<true, false>(p, M, N, C, ldc, scale, stream);
       if (e != hipSuccess) return e;
       return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
     }
@@ -662,8 +862,17 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
   }
 }
 
-hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                                float scale, hipStream_t stream) {
+bool fused_split_ok(const float* A, int64_t lda, int64_t K, float scale) {
+  return scaled_kernel_ok(scale) && reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 &&
+         K % kKPad == 0 && lda < (int64_t{1} << 22);
+}
+
+hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
+                               const float* A, int64_t lda, float* C, int64_t ldc, float scale,
+                               hipStream_t stream) {
+  if (!fused_split_ok(A, lda, K, scale)) return hipErrorInvalidValue;
+  const hipError_t e = launch_el<true, true>(p, M, N, C, ldc, scale, stream, A, lda, K);
+  if (e != hipSuccess) return e;
   return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
 }
 
@@ -674,8 +883,8 @@ hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, i
     return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream, true);
   hipError_t e = hipSuccess;
   switch (stages) {
-    case 1: e = launch_el<false>(p, M, N, C, ldc, scale, stream); break;
-    case 2: e = launch_el<true>(p, M, N, C, ldc, scale, stream); break;
+    case 1: e = launch_el<false, false>(p, M, N, C, ldc, scale, stream); break;
+    case 2: e = launch_el<true, false>(p, M, N, C, ldc, scale, stream); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

@@ -133,6 +133,78 @@ __device__ __forceinline__ half8 pk_scale(const half8& x, uint32_t s2) {
   return __builtin_bit_cast(half8, u32x4{r0, r1, r2, r3});
 }
 
+// Half of pk_scale: words 2 * kPart and 2 * kPart + 1 of out = x * s (four
+// halves).  Two VALU instructions overlap one MFMA for free, four do not, so
+// the kernels form s * B_hi in two halves after different MFMAs.
+template <int kPart>
+__device__ __forceinline__ void pk_scale_half(half8& out, const half8& x, uint32_t s2) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_bit_cast(u32x4, x);
+  u32x4 o = __builtin_bit_cast(u32x4, out);
+  uint32_t r0, r1;
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r0) : "s"(s2), "v"(v[2 * kPart]));
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r1) : "s"(s2), "v"(v[2 * kPart + 1]));
+  o[2 * kPart] = r0;
+  o[2 * kPart + 1] = r1;
+  out = __builtin_bit_cast(half8, o);
+}
+
+// The split of Sec. 3.3 (hi = fl16(a), r = a - hi exactly, lo = fl16(r s)) of
+// two FP32 values a0, a1 into one packed word of high halves and one of scaled
+// residuals, five VALU instructions:
+//   kOp 0  v_cvt_pk_f16_f32      hi = fl16(a0), fl16(a1)
+//   kOp 1  v_fma_mix_f32         r[0] = hi.lo * (-1) + a0   (exact: a - hi
+//   kOp 2  v_fma_mix_f32         r[1] = hi.hi * (-1) + a1    fits FP32)
+//   kOp 3  v_fma_mixlo_f16       lo.lo = fl16(r[0] * s + 0)  (r s exact, s a
+//   kOp 4  v_fma_mixhi_f16       lo.hi = fl16(r[1] * s + 0)   power of two; r
+//                                                             is never -0)
+// Each result is one round-to-nearest-even conversion of an exact value with
+// FP16 and FP32 denormals kept, so the words equal those of split_value.
+// One instruction per call (volatile asm), so that the kernels can place each
+// between two MFMAs; `s` is the wave-uniform scale.  kOp 3 defines the whole
+// register (its other half is written by kOp 4), so no earlier value of lo
+// has to be kept.
+template <int kOp>
+__device__ __forceinline__ void split_op(uint32_t& hi, uint32_t& lo, float (&r)[2], float a0,
+                                         float a1, float s) {
+  if constexpr (kOp == 0)
+    asm volatile("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(hi) : "v"(a0), "v"(a1));
+  else if constexpr (kOp == 1)
+    asm volatile("v_fma_mix_f32 %0, %1, -1.0, %2 op_sel_hi:[1,0,0]"
+                 : "=v"(r[0]) : "v"(hi), "v"(a0));
+  else if constexpr (kOp == 2)
+    asm volatile("v_fma_mix_f32 %0, %1, -1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+                 : "=v"(r[1]) : "v"(hi), "v"(a1));
+  else if constexpr (kOp == 3)
+    asm volatile("v_fma_mixlo_f16 %0, %1, %2, 0" : "=v"(lo) : "v"(r[0]), "s"(s));
+  else
+    asm volatile("v_fma_mixhi_f16 %0, %1, %2, 0" : "+v"(lo) : "v"(r[1]), "s"(s));
+}
+
+// The same split with the five instructions issued back to back.
+__device__ __forceinline__ void split_pair_all(uint32_t& hi, uint32_t& lo, float a0, float a1,
+                                               float s) {
+  float r[2];
+  split_op<0>(hi, lo, r, a0, a1, s);
+  split_op<1>(hi, lo, r, a0, a1, s);
+  split_op<2>(hi, lo, r, a0, a1, s);
+  split_op<3>(hi, lo, r, a0, a1, s);
+  split_op<4>(hi, lo, r, a0, a1, s);
+}
+
+// s * x for four of the eight halves of x (words 2 kPart and 2 kPart + 1 of
+// pk_scale), one v_pk_mul_f16 per word: kWord selects the word.
+template <int kWord>
+__device__ __forceinline__ void pk_scale_word(half8& out, const half8& x, uint32_t s2) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_bit_cast(u32x4, x);
+  u32x4 o = __builtin_bit_cast(u32x4, out);
+  uint32_t r;
+  asm volatile("v_pk_mul_f16 %0, %1, %2" : "=v"(r) : "s"(s2), "v"(v[kWord]));
+  o[kWord] = r;
+  out = __builtin_bit_cast(half8, o);
+}
+
 // The same with the accumulator tied to a VGPR quad.
 __device__ __forceinline__ void mfma16_vacc(floatx4& acc, const half8& a, const half8& b) {
   asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "v"(b));

@@ -55,6 +55,26 @@ __device__ __forceinline__ void split_value(float a, float s, uint16_t& hi, uint
   lo = __builtin_bit_cast(uint16_t, l);
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte store that bypasses the caches' retention (the planes are streamed
+// out once and read back by the GEMM much later).
+__device__ __forceinline__ void store_stream(uint16_t* p, u32x4 v) {
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+}
+
+// The split of eight consecutive values into packed hi and lo words.
+__device__ __forceinline__ void split8(const float (&v)[8], float s, u32x4& hv, u32x4& lv) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint16_t h0, l0, h1, l1;
+    split_value(v[2 * e], s, h0, l0);
+    split_value(v[2 * e + 1], s, h1, l1);
+    hv[e] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
+    lv[e] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+  }
+}
+
 // Pre-scaling shift of a row (column) whose largest finite magnitude has the
 // bits `max_bits`: the power of two that brings that magnitude into
 // [2^target, 2^(target+1)); 0 for an all-zero (or all non-finite) line.
@@ -151,20 +171,21 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, hipStream_t stream);
 
-// Elementwise GEMM that reads A as FP32 and splits it in registers
-// (gemm_fused.hip), on a workspace whose B planes and range flag were written
-// by launch_split_b.  Requires A 16-byte aligned, lda % 4 == 0 and K % 4 == 0.
-// When the range flag is set it writes the A planes instead, and
-// launch_gemm_fallback (which must follow on the same stream) computes C.
+// True when the elementwise order can split A inside the GEMM kernel: s is a
+// finite FP16 value (the kernel keeps the s-scaled accumulator), A is 16-byte
+// aligned, lda is a multiple of 4 (16-byte chunks), K a multiple of 64 (the
+// copies never read past a row) and 256 rows of A span less than 4 GiB (per
+// lane 32-bit copy offsets).
+bool fused_split_ok(const float* A, int64_t lda, int64_t K, float scale);
+
+// Elementwise GEMM that reads A as FP32 and splits it in registers inside the
+// 256 x 256 kernel, on a workspace whose B planes and range flag were written
+// by launch_split_b; requires fused_split_ok.  When the range flag is set
+// (some |B_hi| s > 65504) the kernel writes the A planes instead and the
+// unscaled elementwise kernel, launched after it, computes C.
 hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
                                const float* A, int64_t lda, float* C, int64_t ldc, float scale,
                                hipStream_t stream);
-
-// The unscaled elementwise kernel alone; it computes C only when the range
-// flag is set (and returns at once otherwise).  Used after the fused kernel,
-// which is only launched when scaled_kernel_ok(scale).
-hipError_t launch_gemm_fallback(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                                float scale, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).

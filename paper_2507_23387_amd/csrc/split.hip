@@ -17,8 +17,6 @@
 namespace sgc {
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
 // Row-major split.  Thread = 4 consecutive columns of one row; blockIdx.y
 // strides over rows.  kVec: X rows are 16-byte aligned and hi/lo rows 8-byte
 // aligned, so whole quads move as float4 / 8-byte stores.
@@ -58,23 +56,6 @@ __global__ __launch_bounds__(256) void split_rows_kernel(
           lrow[e] = l[e];
         }
     }
-  }
-}
-
-// 16-byte store that bypasses the caches' retention (the planes are streamed
-// out once and read back by the GEMM much later).
-__device__ __forceinline__ void store_stream(uint16_t* p, u32x4 v) {
-  __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
-}
-
-__device__ __forceinline__ void split8(const float (&v)[8], float s, u32x4& hv, u32x4& lv) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    uint16_t h0, l0, h1, l1;
-    split_value(v[2 * e], s, h0, l0);
-    split_value(v[2 * e + 1], s, h1, l1);
-    hv[e] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-    lv[e] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
   }
 }
 

@@ -209,6 +209,29 @@ def test_compute_a_validation(lib):
     assert call(M=0) == 0                          # validation only: a no-op
 
 
+def test_splits_a_in_gemm_rule(lib):
+    """The in-kernel split of A is chosen for the elementwise order with
+    N <= 4096, scale <= 2^15, 16-byte aligned A, lda % 4 == 0 and below 2^22,
+    and K % 64 == 0; everything else, and invalid arguments, gets 0.  The query
+    only looks at A's address."""
+    q = lambda M=512, N=4096, K=1024, A=FAKE, lda=1024, scale=2048.0, order=0: \
+        lib.sgemm_cube_splits_a_in_gemm(M, N, K, A, lda, scale, order)
+    assert q() == 1
+    assert q(N=1) == 1 and q(M=1) == 1 and q(K=64) == 1
+    assert q(scale=32768.0) == 1 and q(scale=1.0) == 1
+    assert q(lda=1028) == 1
+    assert q(N=4097) == 0                      # many tile columns: split pass
+    assert q(order=1) == 0 and q(order=2) == 0  # termwise, cross-terms-first
+    assert q(order=3) == 0 and q(order=-1) == 0
+    assert q(scale=65536.0) == 0                # unscaled kernel
+    assert q(scale=3.0) == 0 and q(scale=0.5) == 0
+    assert q(A=FAKE + 4) == 0                   # A not 16-byte aligned
+    assert q(lda=1026) == 0                     # lda not a multiple of 4
+    assert q(K=1000, lda=1000) == 0             # K not a multiple of 64
+    assert q(lda=1 << 22) == 0
+    assert q(M=0) == 0 and q(N=0) == 0 and q(K=0) == 0 and q(A=0) == 0
+
+
 def test_noalloc_validates_before_device_work(lib):
     """sgemm_cube_noalloc validates like sgemm_cube and refuses problems whose
     workspace exceeds its fixed 64 MiB array, all before any device call."""

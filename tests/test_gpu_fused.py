@@ -1,14 +1,18 @@
-"""The elementwise GEMM that splits A in registers (sgemm_cube_compute_a when
-A is 16-byte aligned and lda, K are multiples of 4) against the path through
-the split kernels and the A planes (sgemm_cube_ws).
+"""The elementwise GEMM that splits A in registers (the 256 x 256 kernel with
+its A copies taken from FP32 A) against the path through the split kernels
+and the A planes (sgemm_cube_prepare + sgemm_cube_compute).
 
-Both paths apply the same MFMA operations to every accumulator in the same
-order (HH, XA, XB per block), so when the in-register split produces the same
-bits as the split kernels (which the split tests pin to the oracle bit for
-bit) the two results are identical bit for bit; the fused result must also
-meet the parity bar against the oracle.  When s * B_hi overflows FP16 the
-fused kernel writes the A planes itself and the unscaled kernel runs: again
-bit-identical to the planes path."""
+sgemm_cube, sgemm_cube_ws and sgemm_cube_compute_a take the fused path where
+sgemm_cube_splits_a_in_gemm says so (the elementwise order, N <= 4096,
+s <= 2^15, A 16-byte aligned, lda a multiple of 4, K a multiple of 64);
+otherwise they split A into the workspace first.  Both
+paths apply the same MFMA operations to every accumulator in the same order
+(HH, XA, XB per block), so when the in-register split produces the same bits
+as the split kernels (which the split tests pin to the oracle bit for bit)
+the results are identical bit for bit; the fused result must also meet the
+parity bar against the oracle.  When s * B_hi overflows FP16 the fused kernel
+writes the A planes itself and the unscaled kernel runs: again bit-identical
+to the planes path."""
 import numpy as np
 import pytest
 
@@ -19,8 +23,13 @@ from tests.helpers import abs_ab, assert_parity
 
 pytestmark = pytest.mark.gpu
 
-SHAPES = [(1, 1, 4), (17, 33, 68), (129, 700, 36), (256, 256, 256), (300, 200, 1000),
-          (513, 640, 192), (200, 129, 4100)]
+# K a multiple of 64 and N <= 4096 (fused), with ragged M and N; the last
+# three take the planes path (K not a multiple of 64, N above 4096) and must
+# agree all the same.
+SHAPES = [(1, 1, 64), (17, 33, 128), (129, 700, 64), (256, 256, 256), (300, 200, 1024),
+          (513, 640, 192), (200, 129, 4096), (40, 4096, 128), (17, 33, 68), (300, 200, 1000),
+          (40, 4097, 128)]
+FUSED = {shape: shape[2] % 64 == 0 and shape[1] <= 4096 for shape in SHAPES}
 
 
 def _kb():
@@ -29,29 +38,44 @@ def _kb():
     return binding.sgemm_cube_block_k()
 
 
-def _both_paths(A, B, scale=2048.0):
-    """(C through prepare(A = NULL, B) + compute_a(A), C through sgemm_cube_ws)."""
+def _paths(A, B, scale=2048.0, lda=None):
+    """(C through sgemm_cube_ws, C through prepare(A = NULL, B) + compute_a(A),
+    C through prepare(A, B) + compute on the planes)."""
     import torch
 
     from paper_2507_23387_amd import binding
 
     M, K = A.shape
     N = B.shape[1]
-    dA, dB = to_dev(A), to_dev(B)
+    lda = K if lda is None else lda
+    buf = torch.zeros((M * lda + 4,), dtype=torch.float32, device="cuda")
+    dA = buf[:M * lda].view(M, lda)
+    dA[:, :K].copy_(torch.from_numpy(A))
+    dB = to_dev(B)
     stream = torch.cuda.current_stream().cuda_stream
     ws = binding.workspace(M, N, K)
-    Cf = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
-    Cp = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
-    assert binding.sgemm_cube_prepare(M, N, K, None, K, dB.data_ptr(), N, scale,
-                                      ws.data_ptr(), ws.numel(), stream) == 0
-    assert binding.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), K, Cf.data_ptr(), N, scale,
-                                        binding.ELEMENTWISE, ws.data_ptr(), ws.numel(),
-                                        stream) == 0
-    assert binding.sgemm_cube_ws(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, Cp.data_ptr(), N,
-                                 scale, binding.ELEMENTWISE, ws.data_ptr(), ws.numel(),
-                                 stream) == 0
+    n = ws.numel()
+    C = [torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda") for _ in range(3)]
+    assert binding.sgemm_cube_ws(M, N, K, dA.data_ptr(), lda, dB.data_ptr(), N, C[0].data_ptr(),
+                                 N, scale, binding.ELEMENTWISE, ws.data_ptr(), n, stream) == 0
+    assert binding.sgemm_cube_prepare(M, N, K, None, lda, dB.data_ptr(), N, scale,
+                                      ws.data_ptr(), n, stream) == 0
+    assert binding.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), lda, C[1].data_ptr(), N, scale,
+                                        binding.ELEMENTWISE, ws.data_ptr(), n, stream) == 0
+    assert binding.sgemm_cube_prepare(M, N, K, dA.data_ptr(), lda, dB.data_ptr(), N, scale,
+                                      ws.data_ptr(), n, stream) == 0
+    assert binding.sgemm_cube_compute(M, N, K, C[2].data_ptr(), N, scale, binding.ELEMENTWISE,
+                                      ws.data_ptr(), n, stream) == 0
     torch.cuda.synchronize()
-    return Cf.cpu().numpy(), Cp.cpu().numpy()
+    return [c.cpu().numpy() for c in C]
+
+
+def _both_paths(A, B, scale=2048.0, lda=None):
+    """(fused C, planes C), after checking that sgemm_cube_ws and compute_a
+    agree bit for bit."""
+    Cw, Ca, Cp = _paths(A, B, scale, lda)
+    _same_bits(Cw, Ca)
+    return Cw, Cp
 
 
 def _same_bits(X, Y):
@@ -77,6 +101,11 @@ def test_fused_split_gives_the_bits_of_the_planes_path(gpu, shape):
     M, N, K = shape
     A, B = _mixed_operands(M, N, K, M + 3 * N + K)
     log(f"fused vs planes {M}x{N}x{K}")
+    from paper_2507_23387_amd import binding
+
+    dA = to_dev(A)
+    assert binding.sgemm_cube_splits_a_in_gemm(M, N, K, dA.data_ptr(), K, 2048.0,
+                                               binding.ELEMENTWISE) == int(FUSED[shape])
     Cf, Cp = _both_paths(A, B)
     _same_bits(Cf, Cp)
     Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
@@ -115,7 +144,7 @@ def test_identity_b_reconstructs_every_split_of_a(gpu):
 def test_fused_range_switch(gpu, edge):
     """|B_hi| s at 65504 keeps the scaled kernel; one FP16 ulp above makes the
     fused kernel write the A planes and the unscaled kernel compute C."""
-    M, N, K = 300, 260, 260
+    M, N, K = 300, 260, 256
     A, B = workloads.make_operands(M, N, K, 22, "uniform_pm1")
     B[5, 7] = 31.984375 if edge == "scaled_limit" else 32.0
     log(f"fused range switch {edge}")
@@ -126,12 +155,14 @@ def test_fused_range_switch(gpu, edge):
 
 
 def test_fused_non_finite_inputs(gpu):
-    M, N, K = 40, 50, 72
+    M, N, K = 40, 50, 128
     A, B = workloads.make_operands(M, N, K, 23, "uniform_pm1")
     A[3, 5] = 70000.0      # hi overflows
     A[7, 9] = -np.inf
     A[20, 21] = 32784.0    # lo overflows with s = 2^12
-    A[30, 71] = np.nan     # in the last k-step's tail
+    A[30, 127] = np.nan    # in the last k-step
+    A[31, 64] = -0.0
+    A[32, 65] = 2.0**-140  # FP32 subnormal
     log("fused non-finite")
     Cf, Cp = _both_paths(A, B, 4096.0)
     _same_bits(Cf, Cp)
@@ -164,9 +195,23 @@ def test_compute_a_after_prepare_of_b(gpu):
         assert torch.equal(C1, C2)
 
 
+def test_padded_lda_takes_the_fused_path_bitwise(gpu):
+    """lda = K + 4 (rows 16-byte aligned) on ragged M and N, and lda = K + 1
+    (the planes path): both equal the planes path bit for bit."""
+    M, N, K = 133, 71, 320
+    A, B = _mixed_operands(M, N, K, 31)
+    for lda in (K + 4, K + 1):
+        log(f"fused padded lda {lda}")
+        Cf, Cp = _both_paths(A, B, lda=lda)
+        _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), "padded lda")
+
+
 def test_unaligned_a_splits_into_the_workspace(gpu):
     """compute_a with A misaligned by one element, or K not a multiple of 4,
-    splits A into the workspace first; the result equals sgemm_cube's."""
+    splits A into the workspace first; the result equals sgemm_cube's (which
+    takes the fused path for the aligned copy at K = 256)."""
     import torch
 
     from paper_2507_23387_amd import binding
