@@ -18,6 +18,7 @@ import glob
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -47,8 +48,19 @@ def sources():
 _MINREG = ["-mllvm", "-amdgpu-sched-strategy=iterative-minreg"]
 FILE_FLAGS = {
     "gemm.hip": _MINREG,
-    "gemm_fused.hip": _MINREG,
 }
+
+# Host AddressSanitizer + UndefinedBehaviorSanitizer for the checking build
+# (build_sanitized): on the host pass only, each flag behind -Xarch_host; the
+# device code is compiled exactly as in the library.
+SANITIZE_HOST = [
+    "-Xarch_host", "-fsanitize=address",
+    "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=all",
+    "-Xarch_host", "-fno-omit-frame-pointer",
+    "-Xarch_host", "-g",
+]
+SANITIZE_DIR = os.path.join(ROOT, "tests", "sanitize")
 
 _NOISE = "is not a recognized feature for this target"
 
@@ -64,22 +76,60 @@ def _run(cmd, verbose):
         print("\n".join(errlines))
 
 
+def _compile_all(jobs, verbose):
+    """Run the compile commands concurrently (one hipcc process each)."""
+    workers = max(1, min(len(jobs), os.cpu_count() or 1, 8))
+    with ThreadPoolExecutor(max_workers=workers) as pool:
+        for f in [pool.submit(_run, cmd, verbose) for cmd in jobs]:
+            f.result()
+
+
+def _includes():
+    return ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc")]
+
+
 def build(verbose: bool = False, extra_flags=()) -> str:
     """Compile every source to an object (with its FILE_FLAGS) and link them."""
-    incs = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc")]
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     compile_flags = [f for f in FLAGS if f != "-shared"]
-    objs = []
+    jobs, objs = [], []
     for src in sources():
         name = os.path.basename(src)
         obj = os.path.join(objdir, name + ".o")
-        _run([HIPCC, *compile_flags, *FILE_FLAGS.get(name, []), *extra_flags, *incs, "-c", src,
-              "-o", obj], verbose)
+        jobs.append([HIPCC, *compile_flags, *FILE_FLAGS.get(name, []), *extra_flags, *_includes(),
+                     "-c", src, "-o", obj])
         objs.append(obj)
+    _compile_all(jobs, verbose)
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", LIB + ".tmp"], verbose)
     os.replace(LIB + ".tmp", LIB)
     return LIB
+
+
+def build_sanitized(out_dir: str | None = None, verbose: bool = False) -> str:
+    """Build tests/sanitize/abi_check: the library's sources with SANITIZE_HOST
+    on their host pass, linked statically into the program that drives every
+    entry point.  The device code is the library's (same flags, same gfx950
+    kernels).  Returns the path of the executable."""
+    default_dir = os.path.join(SANITIZE_DIR, "_build")
+    out_dir = out_dir or default_dir
+    os.makedirs(out_dir, exist_ok=True)
+    compile_flags = [f for f in FLAGS if f not in ("-shared", "-fvisibility=hidden")]
+    jobs, objs = [], []
+    for src in [*sources(), os.path.join(SANITIZE_DIR, "abi_check.cpp")]:
+        name = os.path.basename(src)
+        obj = os.path.join(out_dir, name + ".o")
+        lang = ["-x", "hip"] if name.endswith(".cpp") else []
+        jobs.append([HIPCC, *compile_flags, *FILE_FLAGS.get(name, []), *SANITIZE_HOST,
+                     *_includes(), *lang, "-c", src, "-o", obj])
+        objs.append(obj)
+    _compile_all(jobs, verbose)
+    # The objects stay in out_dir; the default executable goes beside its
+    # source (build folders do not travel with the tree).
+    exe = os.path.join(SANITIZE_DIR if out_dir == default_dir else out_dir, "abi_check")
+    _run([HIPCC, "--offload-arch=gfx950", *SANITIZE_HOST, *objs, "-o", exe + ".tmp"], verbose)
+    os.replace(exe + ".tmp", exe)
+    return exe
 
 
 if __name__ == "__main__":

@@ -19,6 +19,9 @@ Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base, bool prescale) {
   p.Kp = round_up(K, kKPad);
   const size_t a_bytes = static_cast<size_t>(round_up(p.Mp * p.Kp * 2, 256));
   const size_t b_bytes = static_cast<size_t>(round_up(p.Np * p.Kp * 2, 256));
+  p.bytes = kFlagBytes + 2 * a_bytes + 2 * b_bytes;
+  if (prescale) p.bytes += static_cast<size_t>(round_up((p.Mp + p.Np) * 4, 256));
+  if (!base) return p;  // sizes only
   char* c = static_cast<char*>(base);
   p.range = reinterpret_cast<uint32_t*>(c);
   c += kFlagBytes;
@@ -26,12 +29,10 @@ Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base, bool prescale) {
   p.a_lo = reinterpret_cast<uint16_t*>(c + a_bytes);
   p.b_hi = reinterpret_cast<uint16_t*>(c + 2 * a_bytes);
   p.b_lo = reinterpret_cast<uint16_t*>(c + 2 * a_bytes + b_bytes);
-  p.bytes = kFlagBytes + 2 * a_bytes + 2 * b_bytes;
   if (prescale) {
     // The row and column maxima follow the planes.
     p.row_max = reinterpret_cast<uint32_t*>(c + 2 * a_bytes + 2 * b_bytes);
     p.col_max = p.row_max + p.Mp;
-    p.bytes += static_cast<size_t>(round_up((p.Mp + p.Np) * 4, 256));
   }
   return p;
 }
@@ -233,10 +234,17 @@ int run_allocating(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
   if (need == 0) return run(M, N, K, A, lda, B, ldb, C, ldc, scale, variant, nullptr, stream);
   hipMemPool_t pool = nullptr;
   int st = get_pool(&pool);
-  if (st != SGEMM_CUBE_OK) return st;
+  if (st != SGEMM_CUBE_OK) {
+    (void)hipGetLastError();
+    return st;
+  }
   void* ws = nullptr;
-  if (hipMallocFromPoolAsync(&ws, need, pool, stream) != hipSuccess || !ws)
+  if (hipMallocFromPoolAsync(&ws, need, pool, stream) != hipSuccess || !ws) {
+    // Clear the runtime's last error, so that it is not reported by the
+    // launch check of a later call on this thread.
+    (void)hipGetLastError();
     return SGEMM_CUBE_ERR_ALLOC;
+  }
   st = run(M, N, K, A, lda, B, ldb, C, ldc, scale, variant, ws, stream);
   if (hipFreeAsync(ws, stream) != hipSuccess && st == SGEMM_CUBE_OK) st = SGEMM_CUBE_ERR_HIP;
   return st;

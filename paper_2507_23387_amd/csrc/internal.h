@@ -123,6 +123,8 @@ struct RangeOpts {
   int exp_b = 0;
 };
 
+// Workspace layout for an M x N x K problem carved from `base`.  With base
+// null only the sizes (Mp, Np, Kp, bytes) are filled and every pointer is null.
 Planes plan_planes(int64_t M, int64_t N, int64_t K, void* base, bool prescale = false);
 
 // Enqueue the split of a rows x cols row-major FP32 matrix into row-major
