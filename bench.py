@@ -55,6 +55,16 @@ GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true, true>",
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
+def gemm_kernel_name(kernel_key: str) -> str:
+    """Kernel name of a GEMM_KERNELS key or of "elementwise_tile_BMxBNxBK"
+    (the tile sweep: two workgroups per compute unit for 128x128x32)."""
+    if kernel_key.startswith("elementwise_tile_"):
+        bm, bn, bk = (int(v) for v in kernel_key.rsplit("_", 1)[1].split("x"))
+        occ = 2 if (bm, bn, bk) == (128, 128, 32) else 1
+        return f"gemm_tile_kernel<{bm}, {bn}, {bk}, {occ}>"
+    return GEMM_KERNELS[kernel_key]
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -88,7 +98,8 @@ def kernel_source_hash() -> str:
     built from: ties a committed HBM-traffic measurement to the kernel it was
     taken on."""
     h = hashlib.sha256()
-    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/gemm_common.h",
+    for rel in ("paper_2507_23387_amd/csrc/gemm.hip", "paper_2507_23387_amd/csrc/gemm_tile.hip",
+                "paper_2507_23387_amd/csrc/gemm_common.h",
                 "paper_2507_23387_amd/csrc/internal.h"):
         with open(os.path.join(ROOT, rel), encoding="utf-8") as f:
             h.update(_code_only(f.read()).encode())
@@ -285,6 +296,10 @@ def main():
                     help="elementwise only: 2 = copies overlapped with the MFMAs, 1 = copies "
                          "issued and waited for at the end of each step (0 = the library's "
                          "default), through sgemm_cube_compute_stages")
+    ap.add_argument("--tile", default=None,
+                    help="elementwise only: BMxBNxBK, time the tile-sweep kernel of "
+                         "sgemm_cube_compute_tile (256x256x32, 256x128x32, 128x256x32, "
+                         "128x128x32, 128x128x64) instead of the library's GEMM")
     ap.add_argument("--unfused", action="store_true",
                     help="elementwise only: split A into the workspace and run the GEMM on the A "
                          "planes also where sgemm_cube would split A inside the GEMM kernel")
@@ -334,7 +349,12 @@ def main():
     # of B (sgemm_cube_prepare with A = NULL) and sgemm_cube_compute_a; else,
     # and with --unfused or --stages, the split of both operands
     # (sgemm_cube_prepare) and the GEMM on the tiled planes.
-    fused = (not args.unfused and not args.stages and not args.prescale and
+    tile = tuple(int(v) for v in args.tile.lower().split("x")) if args.tile else None
+    if tile and (order != "elementwise" or tile not in sgc.binding.TILE_CONFIGS):
+        print(f"--tile {args.tile}: the sweep covers the elementwise order and "
+              f"{sgc.binding.TILE_CONFIGS}", file=sys.stderr)
+        sys.exit(2)
+    fused = (not args.unfused and not args.stages and not args.prescale and not tile and
              sgc.binding.sgemm_cube_splits_a_in_gemm(M, N, K, dA.data_ptr(), K, scale,
                                                      order_code) == 1)
 
@@ -348,6 +368,9 @@ def main():
         if fused:
             st = sgc.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), K, dC.data_ptr(), N, scale,
                                           order_code, ws.data_ptr(), ws_bytes, sh)
+        elif tile:
+            st = sgc.binding.sgemm_cube_compute_tile(M, N, K, dC.data_ptr(), N, scale, order_code,
+                                                     *tile, ws.data_ptr(), ws_bytes, sh)
         elif args.stages:
             st = sgc.binding.sgemm_cube_compute_stages(M, N, K, dC.data_ptr(), N, scale,
                                                        order_code, args.stages, ws.data_ptr(),
@@ -431,12 +454,14 @@ def main():
         hdr = ws[:8].view(torch.int32).cpu()
         if bool(hdr[0] == hdr[1]) or scale > 32768.0:
             kernel_key = "elementwise_unscaled"
+        elif tile:
+            kernel_key = "elementwise_tile_" + "x".join(map(str, tile))
         elif not fused:
             kernel_key = "elementwise_unfused"
     traffic = traffic_entry(w.name, kernel_key)
     roofline = {
         "bound": "mfma",
-        "kernel": GEMM_KERNELS[kernel_key],
+        "kernel": gemm_kernel_name(kernel_key),
         "achieved": gemm_tflops,
         "peak": FP16_PEAK_TFLOPS,
         "unit": "TFLOP/s",
@@ -540,7 +565,8 @@ def main():
                    "distribution": w.dist, "scale": scale, "order": order,
                    **({"prescale": True} if args.prescale else {}),
                    "split_of_a": "in the GEMM kernel" if fused else "separate pass",
-                   **({"stages": args.stages} if args.stages else {})},
+                   **({"stages": args.stages} if args.stages else {}),
+                   **({"tile": "x".join(map(str, tile))} if tile else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "parity": parity,

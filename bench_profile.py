@@ -99,8 +99,8 @@ def traffic(fetch_dir, write_dir, workload, order, copy_mib):
     w_copy = max(_find(write, "copyBuffer"))
     f_scale = copy_kib / f_copy
     w_scale = copy_kib / w_copy
-    kname = bench.GEMM_KERNELS[order].split("<")[0]
-    tmpl = bench.GEMM_KERNELS[order].split("<")[1].rstrip(">")
+    kname = bench.gemm_kernel_name(order).split("<")[0]
+    tmpl = bench.gemm_kernel_name(order).split("<")[1].rstrip(">")
     key = f"{kname}<{tmpl}"  # template argument as in the mangled-free name
     gf = [v for k, vs in fetch.items() if kname in k and f"<{tmpl}" in k for v in vs]
     gw = [v for k, vs in write.items() if kname in k and f"<{tmpl}" in k for v in vs]

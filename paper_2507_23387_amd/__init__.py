@@ -26,6 +26,7 @@ _EXPORTS = (
     "sgemm_cube_compute",
     "sgemm_cube_compute_a",
     "sgemm_cube_compute_stages",
+    "sgemm_cube_compute_tile",
     "sgemm_cube_ex",
     "sgemm_cube_ex_workspace_size",
     "sgemm_cube_hgemm",

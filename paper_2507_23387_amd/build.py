@@ -48,6 +48,7 @@ def sources():
 _MINREG = ["-mllvm", "-amdgpu-sched-strategy=iterative-minreg"]
 FILE_FLAGS = {
     "gemm.hip": _MINREG,
+    "gemm_tile.hip": _MINREG,
 }
 
 # Host AddressSanitizer + UndefinedBehaviorSanitizer for the checking build

@@ -278,15 +278,19 @@ int scratch_address(void** out) {
   return SGEMM_CUBE_OK;
 }
 
-// sgemm_cube_compute and sgemm_cube_compute_stages; stages == 0 means the
-// library's default pipeline.
+// sgemm_cube_compute, sgemm_cube_compute_stages and sgemm_cube_compute_tile;
+// stages == 0 and tile_m == 0 mean the library's default kernels.
 int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale, int accum_order,
-            int stages, const void* ws, size_t ws_bytes, hipStream_t stream) {
+            int stages, const void* ws, size_t ws_bytes, hipStream_t stream, int tile_m = 0,
+            int tile_n = 0, int block_k = 0) {
   if (!valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !valid_scale(scale))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (stages < 0 || stages > 2) return SGEMM_CUBE_ERR_INVALID_VALUE;
-  if (stages != 0 && accum_order != SGEMM_CUBE_ELEMENTWISE) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  const bool tile = tile_m != 0 || tile_n != 0 || block_k != 0;
+  if (tile && !tile_config_ok(tile_m, tile_n, block_k)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if ((stages != 0 || tile) && accum_order != SGEMM_CUBE_ELEMENTWISE)
+    return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   if (round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   if (M == 0 || N == 0) return SGEMM_CUBE_OK;
@@ -299,7 +303,8 @@ int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
   if (overlap(ws, need, C, span_bytes(M, N, ldc, 4))) return SGEMM_CUBE_ERR_INVALID_VALUE;
   const Planes p = plan_planes(M, N, K, const_cast<void*>(ws));
   const hipError_t e =
-      stages == 0
+      tile ? launch_gemm_tile(p, M, N, C, ldc, scale, tile_m, tile_n, block_k, stream)
+      : stages == 0
           ? launch_gemm(p, M, N, C, ldc, scale, variant_of(accum_order), stream)
           : launch_gemm_stages(p, M, N, C, ldc, scale, stages, stream);
   return e == hipSuccess ? SGEMM_CUBE_OK : SGEMM_CUBE_ERR_HIP;
@@ -467,6 +472,14 @@ int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t
                               size_t ws_bytes, hipStream_t stream) {
   if (stages < 1) return SGEMM_CUBE_ERR_INVALID_VALUE;
   return sgc::compute(M, N, K, C, ldc, scale, accum_order, stages, ws, ws_bytes, stream);
+}
+
+int sgemm_cube_compute_tile(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
+                            int accum_order, int tile_m, int tile_n, int block_k, const void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  if (tile_m == 0 && tile_n == 0 && block_k == 0) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  return sgc::compute(M, N, K, C, ldc, scale, accum_order, 0, ws, ws_bytes, stream, tile_m,
+                      tile_n, block_k);
 }
 
 size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order) {

@@ -876,6 +876,11 @@ hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
   return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
 }
 
+hipError_t launch_gemm_unscaled(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                                float scale, bool only, hipStream_t stream) {
+  return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream, only);
+}
+
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, hipStream_t stream) {
   if (stages < 1 || stages > 2) return hipErrorInvalidValue;

@@ -173,6 +173,22 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
 hipError_t launch_gemm_stages(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
                               float scale, int stages, hipStream_t stream);
 
+// The unscaled elementwise kernel alone (only = true: it computes C whatever
+// the range flag says) or after a scaled kernel (only = false: it computes C
+// when the range flag is set and returns at once otherwise).
+hipError_t launch_gemm_unscaled(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                                float scale, bool only, hipStream_t stream);
+
+// The tile-shape and k-depth sweep of the scaled elementwise kernel
+// (gemm_tile.hip): tile_m x tile_n tiles of C with block_k of k per pipeline
+// stage, one of the configurations tile_config_ok accepts; the same bits as
+// launch_gemm's elementwise order.  Scales above 2^15 and a set range flag
+// take the unscaled kernel, as there.
+bool tile_config_ok(int tile_m, int tile_n, int block_k);
+hipError_t launch_gemm_tile(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
+                            float scale, int tile_m, int tile_n, int block_k,
+                            hipStream_t stream);
+
 // True when the elementwise order can split A inside the GEMM kernel: s is a
 // finite FP16 value (the kernel keeps the s-scaled accumulator), A is 16-byte
 // aligned, lda is a multiple of 4 (16-byte chunks), K a multiple of 64 (the

@@ -189,6 +189,19 @@ def test_compute_stages_validation(lib):
 
 
 
+def test_compute_tile_validation(lib):
+    ws = FAKE + (3 << 30)
+    call = lambda order=0, tm=256, tn=256, bk=32, M=4: lib.sgemm_cube_compute_tile(
+        M, 4, 4, FAKE, 4, 2048.0, order, tm, tn, bk, ws, 1 << 20, 0)
+    assert call(tm=0, tn=0, bk=0) == INVALID
+    for cfg in ((64, 64, 32), (256, 256, 64), (256, 128, 64), (128, 128, 16), (384, 128, 32)):
+        assert call(tm=cfg[0], tn=cfg[1], bk=cfg[2]) == INVALID, cfg
+    assert call(order=1) == NOT_SUPPORTED
+    assert call(order=3) == INVALID
+    for cfg in lib.TILE_CONFIGS:
+        assert call(M=0, tm=cfg[0], tn=cfg[1], bk=cfg[2]) == 0   # validation only
+
+
 def test_compute_a_validation(lib):
     A, C, ws = FAKE, FAKE + (2 << 30), FAKE + (3 << 30)
     call = lambda M=4, N=4, K=4, A=A, lda=4, C=C, ldc=4, scale=2048.0, order=0, ws=ws, \
