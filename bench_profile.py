@@ -4,7 +4,7 @@
         kernel statistics of a `rocprofv3 --kernel-trace --stats` run
         (DIR/**/*kernel_stats.csv) as a markdown table
     python bench_profile.py traffic FETCH_DIR WRITE_DIR --workload W --order O
-                            [--copy-mib 512]
+                            [--copy-mib 512] [--source profiles/FILE.md]
         HBM traffic of the GEMM kernel from two `rocprofv3 --pmc` passes
         (FETCH_SIZE, then WRITE_SIZE), each scaled by what the same counter
         reads for bench.py's plain device copy of --copy-mib MiB; writes the
@@ -88,7 +88,7 @@ def _find(per: dict, needle: str):
     return per[hits[0]]
 
 
-def traffic(fetch_dir, write_dir, workload, order, copy_mib):
+def traffic(fetch_dir, write_dir, workload, order, copy_mib, source=None):
     w = workloads.get(workload)
     fetch = counters(fetch_dir, "FETCH_SIZE")
     write = counters(write_dir, "WRITE_SIZE")
@@ -113,7 +113,7 @@ def traffic(fetch_dir, write_dir, workload, order, copy_mib):
     alg = alg_read + 4 * M * N
     entry = {"bytes": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
              "algorithmic_bytes": alg, "fetch_scale": f_scale, "write_scale": w_scale,
-             "source": f"profiles/hbm_traffic_{workload}_{order}.md"}
+             "source": source or f"profiles/hbm_traffic_{workload}_{order}.md"}
     try:
         with open(bench.TRAFFIC_FILE) as fh:
             data = json.load(fh)
@@ -206,6 +206,9 @@ def main():
     b.add_argument("--workload", default="square8192_uniform")
     b.add_argument("--order", default="elementwise")
     b.add_argument("--copy-mib", type=int, default=512)
+    b.add_argument("--source", default=None,
+                   help="the profiles/ summary the entry cites (default "
+                        "profiles/hbm_traffic_<workload>_<order>.md)")
     c = sub.add_parser("busy")
     c.add_argument("dir")
     d = sub.add_parser("lds_l2")
@@ -215,7 +218,7 @@ def main():
         print(stats(args.dir))
     elif args.cmd == "traffic":
         print(traffic(args.fetch_dir, args.write_dir, workloads.get(args.workload).name,
-                      args.order, args.copy_mib))
+                      args.order, args.copy_mib, args.source))
     elif args.cmd == "busy":
         print(busy(args.dir))
     else:

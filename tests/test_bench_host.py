@@ -84,9 +84,12 @@ def test_committed_traffic_file_is_consistent():
     with open(os.path.join(ROOT, "profiles", "gemm_traffic.json")) as f:
         data = json.load(f)
     assert len(data["kernel_source_hash"]) == 16
-    e = data["entries"]["square8192_uniform/elementwise"]
-    assert e["bytes"] == pytest.approx(e["fetch_bytes"] + e["write_bytes"])
-    # Four FP16 planes of 8192 x 8192 read, C written once in FP32.
+    for key, e in data["entries"].items():
+        assert e["bytes"] == pytest.approx(e["fetch_bytes"] + e["write_bytes"]), key
+        assert os.path.exists(os.path.join(ROOT, e["source"])), (key, e["source"])
+    # The default bench line's kernel at 8192^3 (A split in a pass of its own):
+    # four FP16 planes of 8192 x 8192 read, C written once in FP32.
+    e = data["entries"]["square8192_uniform/elementwise_unfused"]
     assert e["algorithmic_bytes"] == 4 * 8192 * 8192 * 2 + 8192 * 8192 * 4
 
 
