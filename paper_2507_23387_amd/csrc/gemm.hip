@@ -147,6 +147,14 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_el_kernel(
     const float* __restrict__ af, int64_t lda, int K) {
   static_assert(kPrefetch || !kFusedA, "the fused split runs with the overlapped copies only");
   constexpr int kBBase = 2 * kSlotHalves;     // the B slots follow the two A slots
+  // The furthest DMA targets: plane tile 3 of the lo plane of B slot 1, and
+  // of A slot 1 (FP32 rows of the fused split: 4 KiB group 7 of slot 1).
+  static_assert(dma_end_bytes(kBBase + kSlotHalves + kStepPlaneHalves + 3 * kTileHalves) <=
+                    kElLdsBytes && kElLdsBytes <= kMaxLdsBytes, "B DMAs stay in LDS");
+  static_assert(dma_end_bytes(kSlotHalves + kStepPlaneHalves + 3 * kTileHalves) <=
+                    static_cast<size_t>(kBBase) * 2, "A DMAs stay in the A slots");
+  static_assert(static_cast<size_t>(kSlotHalves) * 2 + 7 * 4096 + 4096 <=
+                    static_cast<size_t>(kBBase) * 2, "FP32 A DMAs stay in the A slots");
   constexpr int kDmaCols = 4;                 // column blocks that issue the DMAs
   constexpr int kDmaPerCol = 16 / kDmaCols;   // after MFMAs 2, 8, 14, 20 of a block
   int tm, tn;
@@ -415,6 +423,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
     int tiles_n, float* __restrict__ C, int64_t ldc, int M, int N) {
   constexpr int kStageHalves = 2 * kStepPlaneHalves;  // A_hi, B_hi
   constexpr int kDma = 8;                             // 1 KiB DMAs per wave per stage
+  static_assert(dma_end_bytes(kStageHalves + kStepPlaneHalves + 3 * kTileHalves) <=
+                    kHiLdsBytes && kHiLdsBytes <= kMaxLdsBytes, "DMAs stay in LDS");
   extern __shared__ __align__(16) uint16_t lds[];
 
   int tm, tn;
@@ -550,6 +560,10 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   constexpr int kAPlane = kTwM * kStep;      // one A plane of one step: 16 KiB
   constexpr int kBPlane = kTwN * kStep;      // one B plane of one step: 8 KiB
   constexpr int kBBase = 2 * kTwASlot;       // the B slots follow the two A slots
+  static_assert(dma_end_bytes(kTwASlot + kAPlane + 3 * kTileHalves) <=
+                    static_cast<size_t>(kBBase) * 2, "A DMAs stay in the A slots");
+  static_assert(dma_end_bytes(kBBase + kTwBSlot + kBPlane + kTileHalves) <= kTwLdsBytes &&
+                    kTwLdsBytes <= kMaxLdsBytes, "B DMAs stay in LDS");
   if constexpr (V == kElementwise) {
     // Unless the host routed the call here (unscaled_only: s is not a finite
     // FP16 value), the scaled 256 x 256 kernel handles the case where the

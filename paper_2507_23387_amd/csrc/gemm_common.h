@@ -37,6 +37,16 @@ __device__ __forceinline__ void dma16s(const void* base, unsigned voff, unsigned
   asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sb), "{m0}"(lds_addr) : "memory");
 }
 
+// Byte just past the furthest LDS DMA target of a kernel whose DMAs write
+// 4 KiB plane tiles (each wave of four copying its 1 KiB block of the tile)
+// at LDS halves offsets up to `last_tile_halves`.  The kernels check this
+// against their dynamic LDS size, and against the 128 KiB that every DMA
+// target stays below, at compile time.
+constexpr size_t dma_end_bytes(int last_tile_halves) {
+  return static_cast<size_t>(last_tile_halves) * 2 + static_cast<size_t>(kTileHalves) * 2;
+}
+constexpr size_t kMaxLdsBytes = 128 * 1024;
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");

@@ -51,7 +51,13 @@ struct TileShape {
   static constexpr size_t kLdsBytes = static_cast<size_t>(2) * (kASlot + kBSlot) * 2;
   static_assert(kBM % kPanel == 0 && kBN % kPanel == 0, "tiles are whole 128-row panels");
   static_assert(kBK % kTileStep == 0 && kKPad % kBK == 0, "stages divide the padded K");
-  static_assert(kLdsBytes <= 128 * 1024, "LDS of every kernel stays within 128 KiB");
+  static_assert(kLdsBytes <= kMaxLdsBytes, "LDS of every kernel stays within 128 KiB");
+  // The furthest DMA targets: the last tile of the lo plane of slot 1 of A
+  // (before the B slots) and of B (the end of LDS).
+  static_assert(dma_end_bytes(kASlot + kAPlane + (kPA * kSL - 1) * kTileHalves) <=
+                    static_cast<size_t>(kBBase) * 2, "A DMAs stay in the A slots");
+  static_assert(dma_end_bytes(kBBase + kBSlot + kBPlane + (kPB * kSL - 1) * kTileHalves) <=
+                    kLdsBytes, "B DMAs stay in LDS");
 };
 
 // Halves offset, within one plane of one stage, of this lane's fragment of

@@ -154,6 +154,23 @@ def test_fused_range_switch(gpu, edge):
     assert_parity(Cf, Co, K, abs_ab(A, B), f"fused range switch {edge}")
 
 
+@pytest.mark.parametrize("s_b", [0, 13, 15])
+def test_fused_split_at_other_scales(gpu, s_b):
+    """The in-kernel split at s = 1, 2^13 and 2^15 (the largest scale the
+    scaled kernel takes; |B| < 1 keeps the range flag clear), with A values
+    whose hi is FP16-subnormal and whose scaled residual is subnormal."""
+    M, N, K = 257, 300, 192
+    A, B = workloads.make_operands(M, N, K, 30 + s_b, "uniform_pm1")
+    A[::3] *= np.float32(2.0**-16)
+    B *= np.float32(0.999)
+    scale = 2.0**s_b
+    log(f"fused split at s = 2^{s_b}")
+    Cf, Cp = _both_paths(A, B, scale)
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, scale, "elementwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), f"fused s=2^{s_b}")
+
+
 def test_fused_non_finite_inputs(gpu):
     M, N, K = 40, 50, 128
     A, B = workloads.make_operands(M, N, K, 23, "uniform_pm1")
