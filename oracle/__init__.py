@@ -22,7 +22,11 @@ Functions and what pins them (see tests/test_oracle_*.py):
   have no printed bound: each is also pinned, by brute force in exact
   rationals, to the standard summation bound gamma_d * sum|terms| around the
   exact three-term sum, d the order's longest rounding chain
-  (bounds.elementwise_depth, bounds.cross_first_depth).
+  (bounds.elementwise_depth, bounds.cross_first_depth).  The multi-block
+  folds of all three orders are pinned exactly by tests/golden/fold_orders.txt:
+  hand-worked dot products of three blocks whose every rounding step the test
+  re-derives with single binary32 operations, chosen so that the three orders
+  and a plausible misreading of each give different bits.
 * ``prescale_exponents`` / ``sgemm_prescaled`` / ``range_classes``: the
   range extensions the paper names without fixing a rule (exponent
   management of the high part, Sec. 4.2; input-dependent scaling and an
