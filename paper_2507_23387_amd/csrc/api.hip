@@ -462,6 +462,9 @@ int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_
 int sgemm_cube_splits_a_in_gemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                                 float scale, int accum_order) {
   if (M <= 0 || N <= 0 || K <= 0 || !A || !sgc::valid_scale(scale)) return 0;
+  if (lda < K || !sgc::ld_ok(M, lda) || M > sgc::kMaxDim || N > sgc::kMaxDim ||
+      K > sgc::kMaxDim || sgc::round_up_tiles_exceed(M, N))
+    return 0;
   if (accum_order < SGEMM_CUBE_ELEMENTWISE || accum_order > SGEMM_CUBE_ELEMENTWISE_CROSS_FIRST)
     return 0;
   return sgc::splits_a_in_gemm(N, A, lda, K, scale, sgc::variant_of(accum_order)) ? 1 : 0;

@@ -242,6 +242,8 @@ def test_splits_a_in_gemm_rule(lib):
     assert q(lda=1026) == 0                     # lda not a multiple of 4
     assert q(K=1000, lda=1000) == 0             # K not a multiple of 64
     assert q(lda=1 << 22) == 0
+    assert q(lda=512) == 0                      # lda < K: the calls reject it
+    assert q(M=(1 << 30) + 1) == 0              # beyond the indexing limits
     assert q(M=0) == 0 and q(N=0) == 0 and q(K=0) == 0 and q(A=0) == 0
 
 
