@@ -10,13 +10,15 @@
 //   gemm_el_kernel   256 x 256 tiles, v_mfma_f32_16x16x32_f16: the scaled
 //                    elementwise order (Eq. elementwise, Sec. 4.5), one
 //                    accumulator holding s * acc, blocks of one 32-wide
-//                    k-step.
+//                    k-step; on the A planes, or (kFusedA) on FP32 A that it
+//                    splits in registers (Sec. 3.3).
 //   gemm_n128_kernel 256 x 128 tiles, v_mfma_f32_16x16x32_f16: the orders
 //                    that need three accumulator sets -- termwise (Eq.
 //                    termwise), the unscaled elementwise fallback (range
 //                    flag set) and the cross-terms-first order (end of
 //                    Sec. 4.5).
 //   gemm_hi_kernel   256 x 256 tiles: HH only, the native-FP16 baseline.
+// The tile-shape sweep of the scaled elementwise order is in gemm_tile.hip.
 // For the elementwise order with s <= 2^15 both elementwise kernels are
 // launched; each reads the range flag first and the one that does not apply
 // returns at once.  For s > 2^15, which is not a finite FP16 value, the host
