@@ -46,12 +46,15 @@ HBM_PEAK_GBS = 8000.0
 # sgemm_cube_splits_a_in_gemm) or the one that reads the A planes (elsewhere,
 # and with --unfused); either call also launches
 # the unscaled 256 x 128 kernel, which reads the range flag and returns at once
-# unless some |B_hi| s exceeds 65504, in which case it does the work.
+# unless some |B_hi| s exceeds 65504, in which case it does the work.  For
+# termwise the 256 x 128 kernel, likewise with A split in registers where the
+# library chooses it.
 GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true, true>",
                 "elementwise_unfused": "gemm_el_kernel<true, false>",
-                "elementwise_unscaled": "gemm_n128_kernel<0>",
-                "termwise": "gemm_n128_kernel<1>",
-                "elementwise_cross_first": "gemm_n128_kernel<3>"}
+                "elementwise_unscaled": "gemm_n128_kernel<0, false>",
+                "termwise": "gemm_n128_kernel<1, false>",
+                "termwise_fused": "gemm_n128_kernel<1, true>",
+                "elementwise_cross_first": "gemm_n128_kernel<3, false>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
@@ -301,8 +304,8 @@ def main():
                          "sgemm_cube_compute_tile (256x256x32, 256x128x32, 128x256x32, "
                          "128x128x32, 128x128x64) instead of the library's GEMM")
     ap.add_argument("--unfused", action="store_true",
-                    help="elementwise only: split A into the workspace and run the GEMM on the A "
-                         "planes also where sgemm_cube would split A inside the GEMM kernel")
+                    help="split A into the workspace and run the GEMM on the A planes also where "
+                         "sgemm_cube would split A inside the GEMM kernel")
     ap.add_argument("--prescale", action="store_true",
                     help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -458,6 +461,8 @@ def main():
             kernel_key = "elementwise_tile_" + "x".join(map(str, tile))
         elif not fused:
             kernel_key = "elementwise_unfused"
+    elif order == "termwise" and fused:
+        kernel_key = "termwise_fused"
     traffic = traffic_entry(w.name, kernel_key)
     roofline = {
         "bound": "mfma",

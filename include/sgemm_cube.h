@@ -225,10 +225,11 @@ int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_
  * instead of in a pass of its own, else 0 (also for arguments those calls
  * reject).  The in-kernel split repeats the split of each A tile for every
  * tile column of C, so it is chosen only where that costs less than the
- * pass over A: the elementwise order, N <= 4096, scale <= 2^15, A 16-byte
- * aligned, lda a multiple of 4 and below 2^22, and K a multiple of 64.
- * Enqueues nothing and reads no device memory (A is only looked at as an
- * address).  Both choices give the same bits.
+ * pass over A: A 16-byte aligned, lda a multiple of 4 and below 2^22, K a
+ * multiple of 64, and the elementwise order with N <= 4096 and
+ * scale <= 2^15, or the termwise order with N <= 2048 (any scale).  Enqueues nothing and reads no device
+ * memory (A is only looked at as an address).  Both choices give the same
+ * bits.
  */
 int sgemm_cube_splits_a_in_gemm(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                                 float scale, int accum_order);

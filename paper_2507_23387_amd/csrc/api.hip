@@ -136,14 +136,21 @@ RangeOpts range_opts(unsigned options, bool report, float scale) {
 // The in-kernel split of A redoes the split of an A tile once per tile
 // column of C, on the vector ALU between the matrix instructions, while the
 // split pass costs one read of A and one write of its planes through HBM.
-// Measured on MI355X with the elementwise order: the in-kernel split is 13%
-// faster at M x N x K = 16384 x 1024 x 8192, 1% faster at 4096^3 and 4%
-// slower at 8192^3, so it is used up to N = 4096.
+// Measured on MI355X: for the elementwise order (256-column tiles) the
+// in-kernel split is 13 % faster at M x N x K = 16384 x 1024 x 8192, 1 %
+// faster at 4096^3 and 4 % slower at 8192^3, so it is used up to N = 4096.
+// For termwise (128-column tiles, so twice the repeats per column of C): 10 %
+// faster at 16384 x 1024 x 8192, even at 4096^3 and 4 % slower at 4096 x 4096
+// x 16384, so it is used up to N = 2048.
 constexpr int64_t kFusedSplitMaxN = 4096;
+constexpr int64_t kTermwiseFusedMaxN = 2048;
 
 bool splits_a_in_gemm(int64_t N, const float* A, int64_t lda, int64_t K, float scale,
                       int variant) {
-  return variant == kElementwise && N <= kFusedSplitMaxN && fused_split_ok(A, lda, K, scale);
+  const int64_t max_n = variant == kElementwise ? kFusedSplitMaxN
+                        : variant == kTermwise  ? kTermwiseFusedMaxN
+                                                : 0;
+  return N <= max_n && fused_split_ok(A, lda, K, scale, variant);
 }
 
 // GEMM from FP32 A and a workspace whose B planes are prepared: the 256 x 256
@@ -153,7 +160,7 @@ hipError_t compute_from_a(const Planes& p, int64_t M, int64_t N, int64_t K, cons
                           int64_t lda, float* C, int64_t ldc, float scale, int variant,
                           hipStream_t stream) {
   if (splits_a_in_gemm(N, A, lda, K, scale, variant))
-    return launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, stream);
+    return launch_gemm_fused_a(p, M, N, K, A, lda, C, ldc, scale, variant, stream);
   const hipError_t e = launch_split_a(p, M, K, A, lda, scale, RangeOpts{}, next_stamp(), stream);
   if (e != hipSuccess) return e;
   return launch_gemm(p, M, N, C, ldc, scale, variant, stream);

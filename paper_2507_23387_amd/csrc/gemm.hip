@@ -543,19 +543,42 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // a step and two blocks to land, not five blocks: with planes larger than the
 // last-level cache (K = 16384) the single barrier that waited for all copies
 // of the step left termwise 18 % slower.
+//
+// kFusedA (termwise only): the A slots hold the stage's FP32 rows instead of
+// the A planes (256 rows x 32 k, 32 KiB, copied and swizzled as in the fused
+// elementwise kernel), and each wave splits its 64 rows in registers (Sec.
+// 3.3): during blocks 2-7 of step kt it reads the FP32 fragments of stage
+// kt+1 (two 16-byte reads per 16-row block, all before the barrier of block
+// 7, which the DMAs of step kt+1 into that slot wait behind) and runs the 80
+// vector instructions of the split, at most two between consecutive MFMAs,
+// into the register set of step kt+1.  The last of them comes 10 MFMAs
+// before that set's first use.  The bits are those of the planes path.
 constexpr int kTwM = 256;
 constexpr int kTwN = 128;
 constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
 constexpr int kTwBSlot = 2 * kTwN * kStep;        // halves: B_hi, B_lo of one step
 constexpr size_t kTwLdsBytes = static_cast<size_t>(2) * (kTwASlot + kTwBSlot) * 2;  // 96 KiB
 
-template <int V>
+// Slot (the MFMA of a step, 12 per column block, after which it is issued)
+// of split instruction q (0-79: 16-row block q / 20, instruction q % 20) in
+// the fused termwise kernel: 80 instructions over slots 27-93, so that the
+// first comes three slots after the first fragment read (the reads start
+// after the barrier before block 2, slot 24) and the last 10 MFMAs before the
+// next step's first use.
+constexpr int kTwSplitFirst = 27, kTwSplitLast = 93;
+constexpr int tw_split_slot(int q) {
+  return kTwSplitFirst + q * (kTwSplitLast - kTwSplitFirst + 1) / 80;
+}
+
+template <int V, bool kFusedA = false>
 __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
-    float* __restrict__ C, int64_t ldc, int M, int N, float inv_s, int unscaled_only) {
+    float* __restrict__ C, int64_t ldc, int M, int N, float inv_s, int unscaled_only,
+    const float* __restrict__ af, int64_t lda, float s) {
   static_assert(V == kTermwise || V == kElementwise || V == kCrossFirst, "n128 variants");
+  static_assert(!kFusedA || V == kTermwise, "the fused split of A is built for termwise only");
   constexpr bool kFold = V != kTermwise;
   constexpr int kRows = 4;                   // 16-row blocks per wave
   constexpr int kCols = 8;                   // 16-column blocks per wave
@@ -603,10 +626,33 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     dma16s(src_b[p] + static_cast<int64_t>(2 * tc + sl) * kTileHalves, lane_off,
            lds_base + (kBBase + (t & 1) * kTwBSlot + p * kBPlane + sl * kTileHalves) * 2);
   };
+  // Fused split: an A slot holds the FP32 rows of the stage with the layout
+  // of gemm_el_kernel's (row r's 16-byte chunks at positions q ^ g(r),
+  // g(r) = (r & 3) << 1 | bit 3 of r; DMA n = w + 4d fills rows 8n .. 8n+7;
+  // rows past M repeat row M - 1).
+  unsigned a_voff[kFusedA ? 8 : 1];
+  const float* a_tile = nullptr;
+  if constexpr (kFusedA) {
+    const int row0 = tm * kTwM;
+    const int q = (lane & 7) ^ ((((lane >> 3) & 3) << 1) | (w & 1));
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const int r = min(row0 + 8 * (w + 4 * d) + (lane >> 3), M - 1) - row0;
+      a_voff[d] = static_cast<unsigned>(r * lda * 4 + q * 16);
+    }
+    a_tile = af + static_cast<int64_t>(row0) * lda;
+  }
+  auto dma_af = [&](int t, int d) {
+    const int tc = min(t, ksteps - 1);
+    dma16s(a_tile + static_cast<int64_t>(tc) * kStep, a_voff[d],
+           lds_base + (t & 1) * kTwASlot * 2 + d * 4096);
+  };
   // The d-th of the 12 DMAs of step kt: B stage kt+1, then A stage kt+2.
   auto dma = [&](int kt, int d) {
     if (d < 4)
       dma_b(kt + 1, d);
+    else if constexpr (kFusedA)
+      dma_af(kt + 2, d - 4);
     else
       dma_a(kt + 2, d - 4);
   };
@@ -626,6 +672,45 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     return *reinterpret_cast<const half8*>(lds + kBBase + (t & 1) * kTwBSlot + p * kBPlane +
                                            b_off[j & 1] + j * 16 * kSlice);
   };
+  // Fused split: lane l's FP32 fragment of 16-row block i is row
+  // 64 w + 16 i + l % 16 of the tile, k 8c .. 8c + 7 (c = l / 16): chunks 2c
+  // and 2c + 1 of the row, two 16-byte reads (bits 0, 1 and 3 of the row are
+  // those of l, so the swap is the elementwise kernel's).
+  int af_off[2];
+  const int af_swap = ((lane & 3) << 1) | ((lane >> 3) & 1);
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    af_off[h] = ((lane & 15) * 8 + ((2 * (lane >> 4) + h) ^ af_swap)) * 16;
+  auto rd_af = [&](int t, int i, int h) -> floatx4 {
+    const char* base = reinterpret_cast<const char*>(lds) + (t & 1) * kTwASlot * 2;
+    return *reinterpret_cast<const floatx4*>(base + (64 * w + 16 * i) * 128 + af_off[h]);
+  };
+  const float s_sgpr = __builtin_bit_cast(
+      float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, s)));
+  // Instruction k (0-19) of the split of one 16-row block's eight values f
+  // (f[0]: k 8c .. 8c+3, f[1]: 8c+4 .. 8c+7) into the A_hi and A_lo
+  // fragments h, l, in the order that finishes with f[0] first: the high
+  // words of pairs 0-1, their residuals and scaled residual words (k 2-9),
+  // then the same for pairs 2-3 (k 10-19).
+  auto split_k = [&](auto Kc, half8& h, half8& l, const floatx4 (&f)[2], float (&r)[2][2]) {
+    constexpr int k = decltype(Kc)::value;
+    constexpr int grp = k / 10, kk = k % 10;  // pairs 2 grp, 2 grp + 1
+    constexpr int pair = 2 * grp + (kk < 2 ? kk : ((kk - 2) % 4) / 2);
+    constexpr int op = kk < 2 ? 0 : ((kk - 2) < 4 ? 1 + (kk - 2) % 2 : 3 + (kk - 2) % 2);
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 hv = __builtin_bit_cast(u32x4, h), lv = __builtin_bit_cast(u32x4, l);
+    uint32_t hw = hv[pair], lw = lv[pair];
+    const float a0 = f[pair / 2][2 * (pair % 2)], a1 = f[pair / 2][2 * (pair % 2) + 1];
+    split_op<op>(hw, lw, r[pair % 2], a0, a1, s_sgpr);
+    if constexpr (op == 0) {
+      hv[pair] = hw;
+      h = __builtin_bit_cast(half8, hv);
+    }
+    if constexpr (op >= 3) {
+      lv[pair] = lw;
+      l = __builtin_bit_cast(half8, lv);
+    }
+  };
 
   // Termwise: hh, xa, xb.  Block folds: acc (= hh) and the block sums t1, t2
   // of the current and the previous column block (index: block parity).
@@ -644,16 +729,35 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
       for (int j = 0; j < kCols; ++j) xa[i][j] = xb[i][j] = floatx4{};
   }
 
-  static_for<8>([&](auto n) { dma_a(0, decltype(n)::value); });
-  static_for<8>([&](auto n) { dma_a(1, decltype(n)::value); });
+  if constexpr (kFusedA) {
+    static_for<8>([&](auto n) { dma_af(0, decltype(n)::value); });
+    static_for<8>([&](auto n) { dma_af(1, decltype(n)::value); });
+  } else {
+    static_for<8>([&](auto n) { dma_a(0, decltype(n)::value); });
+    static_for<8>([&](auto n) { dma_a(1, decltype(n)::value); });
+  }
   static_for<4>([&](auto n) { dma_b(0, decltype(n)::value); });
   wait_vmcnt<0>();
   lds_barrier();
   half8 AH[kRows], AL[kRows], NH[kRows], NL[kRows], bh[2], bl[2];
+  // Fused split: F holds the FP32 fragment of one 16-row block from its reads
+  // to the last split instruction that uses it; rr the residuals of two pairs.
+  floatx4 F[2];
+  float rr[2][2];
+  if constexpr (kFusedA) {
 #pragma unroll
-  for (int i = 0; i < kRows; ++i) {
-    AH[i] = rd_a(0, 0, i);
-    AL[i] = rd_a(0, 1, i);
+    for (int i = 0; i < kRows; ++i) {
+      AH[i] = AL[i] = NH[i] = NL[i] = half8{};
+      F[0] = rd_af(0, i, 0);
+      F[1] = rd_af(0, i, 1);
+      static_for<20>([&](auto Kc) { split_k(Kc, AH[i], AL[i], F, rr); });
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kRows; ++i) {
+      AH[i] = rd_a(0, 0, i);
+      AL[i] = rd_a(0, 1, i);
+    }
   }
   bh[0] = rd_b(0, 0, 0);
   bl[0] = rd_b(0, 1, 0);
@@ -773,7 +877,28 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
           if constexpr (m == 1) fold_second(jpp, c, 11, 14);
           if constexpr (m == 2) fold_second(jpp, c, 14, 16);
         }
-        if constexpr (j < kCols - 1 && (m == 1 || m == 7)) {
+        if constexpr (kFusedA) {
+          // Slot P of the step: the reads of 16-row block r's two FP32
+          // halves come after the last use of the previous block's half
+          // (F[0] after its instruction 9, F[1] after 19; block 0 at slot
+          // 24), and each split instruction after the MFMA of its slot.
+          constexpr int P = kRows * 3 * j + m;
+          static_for<kRows>([&](auto Rc) {
+            constexpr int r = decltype(Rc)::value;
+            constexpr int f0 = r == 0 ? 24 : tw_split_slot(20 * (r - 1) + 9) + 1;
+            constexpr int f1 = r == 0 ? 25 : tw_split_slot(20 * (r - 1) + 19) + 1;
+            static_assert(f0 >= 24 && f1 >= 24 && f1 <= 83 && f0 < tw_split_slot(20 * r) &&
+                              f1 < tw_split_slot(20 * r + 10),
+                          "fragment reads after the barrier of block 2, before that of block 7");
+            if constexpr (P == f0) F[0] = rd_af(kt + 1, r, 0);
+            if constexpr (P == f1) F[1] = rd_af(kt + 1, r, 1);
+          });
+          static_for<80>([&](auto Qc) {
+            constexpr int q = decltype(Qc)::value;
+            if constexpr (tw_split_slot(q) == P)
+              split_k(std::integral_constant<int, q % 20>{}, nh[q / 20], nl[q / 20], F, rr);
+          });
+        } else if constexpr (j < kCols - 1 && (m == 1 || m == 7)) {
           constexpr int r = rb + m / 6;
           if constexpr (r < re) {
             if constexpr (r < kRows)
@@ -844,18 +969,20 @@ hipError_t launch_hi(const Planes& p, int64_t M, int64_t N, float* C, int64_t ld
   return hipGetLastError();
 }
 
-template <int V>
+template <int V, bool kFusedA = false>
 hipError_t launch_n128(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
-                       hipStream_t stream, bool unscaled_only = false) {
+                       hipStream_t stream, bool unscaled_only = false,
+                       const float* A = nullptr, int64_t lda = 0) {
   static std::atomic<bool> done[kMaxDevices];
-  const hipError_t attr = set_lds(&gemm_n128_kernel<V>, kTwLdsBytes, done);
+  const hipError_t attr = set_lds(&gemm_n128_kernel<V, kFusedA>, kTwLdsBytes, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kTwM);
   const int tiles_n = static_cast<int>(p.Np / kTwN);
-  hipLaunchKernelGGL((gemm_n128_kernel<V>), dim3(tiles_m * tiles_n), dim3(kWideThreads),
-                     kTwLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo, p.range,
-                     static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc, static_cast<int>(M),
-                     static_cast<int>(N), 1.0f / s, unscaled_only ? 1 : 0);
+  hipLaunchKernelGGL((gemm_n128_kernel<V, kFusedA>), dim3(tiles_m * tiles_n),
+                     dim3(kWideThreads), kTwLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo,
+                     p.range, static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc,
+                     static_cast<int>(M), static_cast<int>(N), 1.0f / s, unscaled_only ? 1 : 0,
+                     A, lda, s);
   return hipGetLastError();
 }
 
@@ -878,15 +1005,19 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
   }
 }
 
-bool fused_split_ok(const float* A, int64_t lda, int64_t K, float scale) {
-  return scaled_kernel_ok(scale) && reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 &&
-         K % kKPad == 0 && lda < (int64_t{1} << 22);
+bool fused_split_ok(const float* A, int64_t lda, int64_t K, float scale, int variant) {
+  const bool layout = reinterpret_cast<uintptr_t>(A) % 16 == 0 && lda % 4 == 0 &&
+                      K % kKPad == 0 && lda < (int64_t{1} << 22);
+  if (variant == kElementwise) return layout && scaled_kernel_ok(scale);
+  return layout && variant == kTermwise;
 }
 
 hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
                                const float* A, int64_t lda, float* C, int64_t ldc, float scale,
-                               hipStream_t stream) {
-  if (!fused_split_ok(A, lda, K, scale)) return hipErrorInvalidValue;
+                               int variant, hipStream_t stream) {
+  if (!fused_split_ok(A, lda, K, scale, variant)) return hipErrorInvalidValue;
+  if (variant == kTermwise)
+    return launch_n128<kTermwise, true>(p, M, N, C, ldc, scale, stream, false, A, lda);
   const hipError_t e = launch_el<true, true>(p, M, N, C, ldc, scale, stream, A, lda, K);
   if (e != hipSuccess) return e;
   return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);

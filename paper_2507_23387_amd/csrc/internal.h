@@ -189,21 +189,22 @@ hipError_t launch_gemm_tile(const Planes& p, int64_t M, int64_t N, float* C, int
                             float scale, int tile_m, int tile_n, int block_k,
                             hipStream_t stream);
 
-// True when the elementwise order can split A inside the GEMM kernel: s is a
-// finite FP16 value (the kernel keeps the s-scaled accumulator), A is 16-byte
-// aligned, lda is a multiple of 4 (16-byte chunks), K a multiple of 64 (the
-// copies never read past a row) and 256 rows of A span less than 4 GiB (per
-// lane 32-bit copy offsets).
-bool fused_split_ok(const float* A, int64_t lda, int64_t K, float scale);
+// True when the order (kElementwise or kTermwise) can split A inside its GEMM
+// kernel: A is 16-byte aligned, lda is a multiple of 4 (16-byte chunks), K a
+// multiple of 64 (the copies never read past a row) and 256 rows of A span
+// less than 4 GiB (per-lane 32-bit copy offsets); for the elementwise order
+// also s <= 2^15 (its kernel keeps the s-scaled accumulator).
+bool fused_split_ok(const float* A, int64_t lda, int64_t K, float scale, int variant);
 
-// Elementwise GEMM that reads A as FP32 and splits it in registers inside the
-// 256 x 256 kernel, on a workspace whose B planes and range flag were written
-// by launch_split_b; requires fused_split_ok.  When the range flag is set
-// (some |B_hi| s > 65504) the kernel writes the A planes instead and the
-// unscaled elementwise kernel, launched after it, computes C.
+// GEMM that reads A as FP32 and splits it in registers, on a workspace whose B
+// planes (and range flag) were written by launch_split_b; requires
+// fused_split_ok.  Elementwise: the 256 x 256 kernel; when the range flag is
+// set (some |B_hi| s > 65504) it writes the A planes instead and the unscaled
+// elementwise kernel, launched after it, computes C.  Termwise: the 256 x 128
+// kernel.
 hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
                                const float* A, int64_t lda, float* C, int64_t ldc, float scale,
-                               hipStream_t stream);
+                               int variant, hipStream_t stream);
 
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).

@@ -225,8 +225,9 @@ def test_compute_a_validation(lib):
 def test_splits_a_in_gemm_rule(lib):
     """The in-kernel split of A is chosen for the elementwise order with
     N <= 4096, scale <= 2^15, 16-byte aligned A, lda % 4 == 0 and below 2^22,
-    and K % 64 == 0; everything else, and invalid arguments, gets 0.  The query
-    only looks at A's address."""
+    and K % 64 == 0, and for termwise with the same layout and N <= 2048 at any
+    valid scale; everything else, and invalid arguments, gets 0.  The query only
+    looks at A's address."""
     q = lambda M=512, N=4096, K=1024, A=FAKE, lda=1024, scale=2048.0, order=0: \
         lib.sgemm_cube_splits_a_in_gemm(M, N, K, A, lda, scale, order)
     assert q() == 1
@@ -234,7 +235,11 @@ def test_splits_a_in_gemm_rule(lib):
     assert q(scale=32768.0) == 1 and q(scale=1.0) == 1
     assert q(lda=1028) == 1
     assert q(N=4097) == 0                      # many tile columns: split pass
-    assert q(order=1) == 0 and q(order=2) == 0  # termwise, cross-terms-first
+    assert q(order=2) == 0                      # cross-terms-first: never
+    assert q(order=1) == 0                      # termwise: N <= 2048 only
+    assert q(order=1, N=2048) == 1              # the 256 x 128 kernel
+    assert q(order=1, N=2048, scale=2.0**24) == 1   # termwise keeps no s B_hi
+    assert q(order=1, N=2049) == 0 and q(order=1, N=2048, K=1000, lda=1000) == 0
     assert q(order=3) == 0 and q(order=-1) == 0
     assert q(scale=65536.0) == 0                # unscaled kernel
     assert q(scale=3.0) == 0 and q(scale=0.5) == 0

@@ -38,7 +38,7 @@ def _kb():
     return binding.sgemm_cube_block_k()
 
 
-def _paths(A, B, scale=2048.0, lda=None):
+def _paths(A, B, scale=2048.0, lda=None, order="elementwise"):
     """(C through sgemm_cube_ws, C through prepare(A = NULL, B) + compute_a(A),
     C through prepare(A, B) + compute on the planes)."""
     import torch
@@ -53,27 +53,28 @@ def _paths(A, B, scale=2048.0, lda=None):
     dA[:, :K].copy_(torch.from_numpy(A))
     dB = to_dev(B)
     stream = torch.cuda.current_stream().cuda_stream
+    code = binding.ORDERS[order]
     ws = binding.workspace(M, N, K)
     n = ws.numel()
     C = [torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda") for _ in range(3)]
     assert binding.sgemm_cube_ws(M, N, K, dA.data_ptr(), lda, dB.data_ptr(), N, C[0].data_ptr(),
-                                 N, scale, binding.ELEMENTWISE, ws.data_ptr(), n, stream) == 0
+                                 N, scale, code, ws.data_ptr(), n, stream) == 0
     assert binding.sgemm_cube_prepare(M, N, K, None, lda, dB.data_ptr(), N, scale,
                                       ws.data_ptr(), n, stream) == 0
     assert binding.sgemm_cube_compute_a(M, N, K, dA.data_ptr(), lda, C[1].data_ptr(), N, scale,
-                                        binding.ELEMENTWISE, ws.data_ptr(), n, stream) == 0
+                                        code, ws.data_ptr(), n, stream) == 0
     assert binding.sgemm_cube_prepare(M, N, K, dA.data_ptr(), lda, dB.data_ptr(), N, scale,
                                       ws.data_ptr(), n, stream) == 0
-    assert binding.sgemm_cube_compute(M, N, K, C[2].data_ptr(), N, scale, binding.ELEMENTWISE,
+    assert binding.sgemm_cube_compute(M, N, K, C[2].data_ptr(), N, scale, code,
                                       ws.data_ptr(), n, stream) == 0
     torch.cuda.synchronize()
     return [c.cpu().numpy() for c in C]
 
 
-def _both_paths(A, B, scale=2048.0, lda=None):
+def _both_paths(A, B, scale=2048.0, lda=None, order="elementwise"):
     """(fused C, planes C), after checking that sgemm_cube_ws and compute_a
     agree bit for bit."""
-    Cw, Ca, Cp = _paths(A, B, scale, lda)
+    Cw, Ca, Cp = _paths(A, B, scale, lda, order)
     _same_bits(Cw, Ca)
     return Cw, Cp
 
@@ -251,3 +252,58 @@ def test_unaligned_a_splits_into_the_workspace(gpu):
         C2 = binding.matmul(to_dev(A), dB, 2048.0, "elementwise")
         torch.cuda.synchronize()
         assert torch.equal(C1, C2)
+
+
+# --- termwise: the 256 x 128 kernel that splits A in registers ----------------
+
+TW_SHAPES = [(1, 1, 64), (17, 33, 128), (129, 700, 64), (300, 200, 1024), (513, 1024, 192),
+             (200, 129, 4096), (40, 2048, 128), (300, 200, 1000), (40, 2049, 128)]
+
+
+@pytest.mark.parametrize("shape", TW_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_termwise_fused_split_gives_the_bits_of_the_planes_path(gpu, shape):
+    """Termwise (Eq. termwise) with the split of A inside the 256 x 128
+    kernel: the same bits as the planes path, and parity with the oracle.
+    K a multiple of 64 and N <= 2048 take the fused kernel; the last two
+    shapes take the planes path and must agree all the same."""
+    from paper_2507_23387_amd import binding
+
+    M, N, K = shape
+    A, B = _mixed_operands(M, N, K, 7 * M + N + K)
+    dA = to_dev(A)
+    fused = K % 64 == 0 and N <= 2048
+    assert binding.sgemm_cube_splits_a_in_gemm(M, N, K, dA.data_ptr(), K, 2048.0,
+                                               binding.TERMWISE) == int(fused)
+    log(f"termwise fused vs planes {M}x{N}x{K}")
+    Cf, Cp = _both_paths(A, B, order="termwise")
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, 2048.0, "termwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), f"termwise fused {shape}")
+
+
+@pytest.mark.parametrize("s_b", [0, 13, 20, 24])
+def test_termwise_fused_split_at_other_scales(gpu, s_b):
+    """Termwise needs no s B_hi, so the in-kernel split runs at every scale,
+    2^24 included; subnormal hi and scaled residuals on a third of the rows."""
+    M, N, K = 257, 300, 192
+    A, B = workloads.make_operands(M, N, K, 60 + s_b, "uniform_pm1")
+    A[::3] *= np.float32(2.0**-16)
+    scale = 2.0**s_b
+    log(f"termwise fused split at s = 2^{s_b}")
+    Cf, Cp = _both_paths(A, B, scale, order="termwise")
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, scale, "termwise", kb=_kb())
+    assert_parity(Cf, Co, K, abs_ab(A, B), f"termwise fused s=2^{s_b}")
+
+
+def test_termwise_fused_non_finite_and_padded_lda(gpu):
+    M, N, K = 133, 71, 320
+    A, B = workloads.make_operands(M, N, K, 61, "uniform_pm1")
+    A[3, 5] = 70000.0      # hi overflows
+    A[7, 9] = np.inf
+    A[11, 300] = np.nan
+    log("termwise fused: non-finite inputs, lda = K + 12")
+    Cf, Cp = _both_paths(A, B, lda=K + 12, order="termwise")
+    _same_bits(Cf, Cp)
+    Co = oracle.sgemm(A, B, 2048.0, "termwise", kb=_kb())
+    _same_bits(np.isfinite(Cf).astype(np.float32), np.isfinite(Co).astype(np.float32))
