@@ -547,10 +547,11 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // kFusedA (termwise only): the A slots hold the stage's FP32 rows instead of
 // the A planes (256 rows x 32 k, 32 KiB, copied and swizzled as in the fused
 // elementwise kernel), and each wave splits its 64 rows in registers (Sec.
-// 3.3): during blocks 2-7 of step kt it reads the FP32 fragments of stage
-// kt+1 (two 16-byte reads per 16-row block, all before the barrier of block
-// 7, which the DMAs of step kt+1 into that slot wait behind) and runs the 80
-// vector instructions of the split, at most two between consecutive MFMAs,
+// 3.3): it waits for A stage kt+1 before block 1 instead of block 2, and
+// during blocks 1-7 of step kt it reads the FP32 fragments of that stage
+// (two 16-byte reads per 16-row block, all before the barrier of block 7,
+// which the DMAs of step kt+1 into that slot wait behind) and runs the 80
+// vector instructions of the split, one between consecutive MFMAs (two once),
 // into the register set of step kt+1.  The last of them comes 10 MFMAs
 // before that set's first use.  The bits are those of the planes path.
 constexpr int kTwM = 256;
@@ -561,11 +562,11 @@ constexpr size_t kTwLdsBytes = static_cast<size_t>(2) * (kTwASlot + kTwBSlot) * 
 
 // Slot (the MFMA of a step, 12 per column block, after which it is issued)
 // of split instruction q (0-79: 16-row block q / 20, instruction q % 20) in
-// the fused termwise kernel: 80 instructions over slots 27-93, so that the
-// first comes three slots after the first fragment read (the reads start
-// after the barrier before block 2, slot 24) and the last 10 MFMAs before the
-// next step's first use.
-constexpr int kTwSplitFirst = 27, kTwSplitLast = 93;
+// the fused termwise kernel: 80 instructions over slots 15-93 (one slot holds
+// two), so that the first comes three slots after the first fragment read
+// (the reads start after the barrier before block 1, slot 12) and the last 10
+// MFMAs before the next step's first use.
+constexpr int kTwSplitFirst = 15, kTwSplitLast = 93;
 constexpr int tw_split_slot(int q) {
   return kTwSplitFirst + q * (kTwSplitLast - kTwSplitFirst + 1) / 80;
 }
@@ -799,6 +800,11 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   // followed by 1-2 of the 16 folds of the previous column block.  DMAs
   // complete in issue order, so a vmcnt wait retires all but the newest.
   constexpr int kDmaPerBlock = 3, kBDmas = 4, kADmas = 8;
+  // The block before which A stage kt+1 (copied during step kt-1) is waited
+  // for: block 2, or block 1 with the fused split, whose reads of that stage
+  // then start one block earlier and leave room for one split instruction per
+  // MFMA.
+  constexpr int kAWaitBlock = kFusedA ? 1 : 2;
   static_assert(kBDmas + kADmas == 4 * kDmaPerBlock && kBDmas <= 2 * kDmaPerBlock,
                 "the B DMAs of a step are issued in blocks 0-1, before its A DMAs");
   auto step = [&](int kt, half8 (&ah)[kRows], half8 (&al)[kRows], half8 (&nh)[kRows],
@@ -806,8 +812,9 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     static_for<kCols>([&](auto J) {
       constexpr int j = decltype(J)::value, c = j & 1;
       constexpr int jp = (j + kCols - 1) % kCols;  // the block folded now
-      if constexpr (j == 2) {
-        wait_vmcnt<2 * kDmaPerBlock>();  // all but blocks 0-1's DMAs: A stage kt+1 is in
+      if constexpr (j == kAWaitBlock) {
+        // All but the DMAs of this step's blocks before it: A stage kt+1 is in.
+        wait_vmcnt<kAWaitBlock * kDmaPerBlock>();
         lds_barrier();
       }
       if constexpr (j == kCols - 1) {
@@ -880,16 +887,18 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
         if constexpr (kFusedA) {
           // Slot P of the step: the reads of 16-row block r's two FP32
           // halves come after the last use of the previous block's half
-          // (F[0] after its instruction 9, F[1] after 19; block 0 at slot
-          // 24), and each split instruction after the MFMA of its slot.
+          // (F[0] after its instruction 9, F[1] after 19; block 0 right
+          // after the barrier before block 1), and each split instruction
+          // after the MFMA of its slot.
           constexpr int P = kRows * 3 * j + m;
+          constexpr int kFirstRead = kRows * 3 * kAWaitBlock;
           static_for<kRows>([&](auto Rc) {
             constexpr int r = decltype(Rc)::value;
-            constexpr int f0 = r == 0 ? 24 : tw_split_slot(20 * (r - 1) + 9) + 1;
-            constexpr int f1 = r == 0 ? 25 : tw_split_slot(20 * (r - 1) + 19) + 1;
-            static_assert(f0 >= 24 && f1 >= 24 && f1 <= 83 && f0 < tw_split_slot(20 * r) &&
-                              f1 < tw_split_slot(20 * r + 10),
-                          "fragment reads after the barrier of block 2, before that of block 7");
+            constexpr int f0 = r == 0 ? kFirstRead : tw_split_slot(20 * (r - 1) + 9) + 1;
+            constexpr int f1 = r == 0 ? kFirstRead + 1 : tw_split_slot(20 * (r - 1) + 19) + 1;
+            static_assert(f0 >= kFirstRead && f1 >= kFirstRead && f1 < kRows * 3 * (kCols - 1) &&
+                              f0 < tw_split_slot(20 * r) && f1 < tw_split_slot(20 * r + 10),
+                          "fragment reads after the barrier of block 1, before that of block 7");
             if constexpr (P == f0) F[0] = rd_af(kt + 1, r, 0);
             if constexpr (P == f1) F[1] = rd_af(kt + 1, r, 1);
           });
