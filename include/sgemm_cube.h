@@ -33,7 +33,9 @@
  *     IEEE inf/NaN in the affected outputs, deterministically (Sec. 3.1 scope).
  *     Entries below 2^-14 have a subnormal hi and lose the 22-bit guarantee of
  *     Eq. split_error (Sec. 4.2); they are still computed as defined.
- *   - Thread-safe; the library keeps no per-call state.
+ *     sgemm_cube_ex adds power-of-two pre-scaling and a range report.
+ *   - Thread-safe; the library keeps no per-call state, except that calls of
+ *     sgemm_cube_noalloc that overlap on one GPU share its fixed workspace.
  */
 #ifndef SGEMM_CUBE_H_
 #define SGEMM_CUBE_H_
