@@ -74,36 +74,49 @@ __device__ __forceinline__ void wide_frag_offsets(int lane, int panel, int (&off
 
 // Split of A into the tiled planes, used when the scaled kernel cannot run
 // and the unscaled kernel that follows needs them: the blocking of the split
-// kernel of A (a block of 16 rows x 128 k per workgroup; lane l of wave w
-// splits 8 consecutive k of row 4w + l / 16, so each row is read as one
-// 512-byte piece and each store fills whole 128-byte lines), the blocks taken
-// in turn by the workgroups of the GEMM grid.  A is 16-byte aligned with lda a
-// multiple of 4 here; rows past M and k past K are written as zeros.
+// kernel of A (a block of 16 rows x 128 k; lane l of wave w splits 8
+// consecutive k of row 4w + l / 16, so each row is read as one 512-byte piece
+// and each store fills whole 128-byte lines), the blocks taken in turn by the
+// workgroups of the GEMM grid.  The GEMM's LDS allows one workgroup per
+// compute unit, so each pass of the loop loads four blocks before it splits
+// and stores them, to keep enough reads in flight.  A is 16-byte aligned with
+// lda a multiple of 4 here; rows past M and k past K are written as zeros.
 __device__ void split_a_planes(const float* __restrict__ A, int64_t lda, int M, int K, int Mp,
                                int Kp, uint16_t* __restrict__ a_hi, uint16_t* __restrict__ a_lo,
                                float s) {
+  constexpr int kUnroll = 4;
   const int lane = threadIdx.x & 63;
   const int kblocks = (Kp + 127) / 128;
   const int64_t blocks = static_cast<int64_t>(Mp / 16) * kblocks;
-  for (int64_t b = blockIdx.x; b < blocks; b += gridDim.x) {
-    const int64_t m = (b / kblocks) * 16 + (threadIdx.x >> 6) * 4 + (lane >> 4);
-    const int64_t k0 = (b % kblocks) * 128 + (lane & 15) * 8;
-    if (k0 >= Kp) continue;
-    float v[8];
-    if (m < M && k0 + 7 < K) {
-      const float4* src = reinterpret_cast<const float4*>(A + m * lda + k0);
-      const float4 f0 = src[0], f1 = src[1];
-      v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
-      v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
-    } else {
+  const int64_t stride = gridDim.x;
+  for (int64_t b0 = blockIdx.x; b0 < blocks; b0 += stride * kUnroll) {
+    float v[kUnroll][8];
+    int64_t m[kUnroll], k0[kUnroll];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? A[m * lda + k0 + e] : 0.0f;
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t b = b0 + u * stride;
+      m[u] = (b / kblocks) * 16 + (threadIdx.x >> 6) * 4 + (lane >> 4);
+      k0[u] = (b % kblocks) * 128 + (lane & 15) * 8;
+      if (b < blocks && m[u] < M && k0[u] + 7 < K) {
+        const float4* src = reinterpret_cast<const float4*>(A + m[u] * lda + k0[u]);
+        const float4 f0 = src[0], f1 = src[1];
+        v[u][0] = f0.x; v[u][1] = f0.y; v[u][2] = f0.z; v[u][3] = f0.w;
+        v[u][4] = f1.x; v[u][5] = f1.y; v[u][6] = f1.z; v[u][7] = f1.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          v[u][e] = (b < blocks && m[u] < M && k0[u] + e < K) ? A[m[u] * lda + k0[u] + e] : 0.0f;
+      }
     }
-    u32x4 hv, lv;
-    split8(v, s, hv, lv);
-    const int64_t idx = tiled_index(m, k0, Kp);
-    store_stream(a_hi + idx, hv);
-    store_stream(a_lo + idx, lv);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      if (b0 + u * stride >= blocks || k0[u] >= Kp) continue;
+      u32x4 hv, lv;
+      split8(v[u], s, hv, lv);
+      const int64_t idx = tiled_index(m[u], k0[u], Kp);
+      store_stream(a_hi + idx, hv);
+      store_stream(a_lo + idx, lv);
+    }
   }
 }
 
