@@ -59,13 +59,21 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
 def gemm_kernel_name(kernel_key: str) -> str:
-    """Kernel name of a GEMM_KERNELS key or of "elementwise_tile_BMxBNxBK"
-    (the tile sweep: two workgroups per compute unit for 128x128x32)."""
+    """Kernel name of a GEMM_KERNELS key or of "elementwise_tile_" + tile_name()
+    (the tile sweep: two workgroups per compute unit for 128x128x32; waves
+    2 x 2, or 2 x 4 for eight)."""
     if kernel_key.startswith("elementwise_tile_"):
-        bm, bn, bk = (int(v) for v in kernel_key.rsplit("_", 1)[1].split("x"))
+        dims = [int(v) for v in kernel_key.rsplit("_", 1)[1].split("x")]
+        bm, bn, bk, waves = dims + [4] * (4 - len(dims))
         occ = 2 if (bm, bn, bk) == (128, 128, 32) else 1
-        return f"gemm_tile_kernel<{bm}, {bn}, {bk}, {occ}>"
+        wm, wn = (2, 4) if waves == 8 else (2, 2)
+        return f"gemm_tile_kernel<{bm}, {bn}, {bk}, {occ}, {wm}, {wn}>"
     return GEMM_KERNELS[kernel_key]
+
+
+def tile_name(tile) -> str:
+    """BMxBNxBK for the four-wave sweep kernels, BMxBNxBKxW otherwise."""
+    return "x".join(map(str, tile if tile[3] != 4 else tile[:3]))
 
 
 def log(msg):
@@ -300,9 +308,10 @@ def main():
                          "issued and waited for at the end of each step (0 = the library's "
                          "default), through sgemm_cube_compute_stages")
     ap.add_argument("--tile", default=None,
-                    help="elementwise only: BMxBNxBK, time the tile-sweep kernel of "
+                    help="elementwise only: BMxBNxBK[xWAVES], time the tile-sweep kernel of "
                          "sgemm_cube_compute_tile (256x256x32, 256x128x32, 128x256x32, "
-                         "128x128x32, 128x128x64) instead of the library's GEMM")
+                         "128x128x32, 128x128x64 with 4 waves; 256x256x32x8) instead of the "
+                         "library's GEMM")
     ap.add_argument("--unfused", action="store_true",
                     help="split A into the workspace and run the GEMM on the A planes also where "
                          "sgemm_cube would split A inside the GEMM kernel")
@@ -353,6 +362,8 @@ def main():
     # and with --unfused or --stages, the split of both operands
     # (sgemm_cube_prepare) and the GEMM on the tiled planes.
     tile = tuple(int(v) for v in args.tile.lower().split("x")) if args.tile else None
+    if tile and len(tile) == 3:
+        tile = tile + (4,)
     if tile and (order != "elementwise" or tile not in sgc.binding.TILE_CONFIGS):
         print(f"--tile {args.tile}: the sweep covers the elementwise order and "
               f"{sgc.binding.TILE_CONFIGS}", file=sys.stderr)
@@ -458,7 +469,7 @@ def main():
         if bool(hdr[0] == hdr[1]) or scale > 32768.0:
             kernel_key = "elementwise_unscaled"
         elif tile:
-            kernel_key = "elementwise_tile_" + "x".join(map(str, tile))
+            kernel_key = "elementwise_tile_" + tile_name(tile)
         elif not fused:
             kernel_key = "elementwise_unfused"
     elif order == "termwise" and fused:
@@ -571,7 +582,7 @@ def main():
                    **({"prescale": True} if args.prescale else {}),
                    "split_of_a": "in the GEMM kernel" if fused else "separate pass",
                    **({"stages": args.stages} if args.stages else {}),
-                   **({"tile": "x".join(map(str, tile))} if tile else {})},
+                   **({"tile": tile_name(tile)} if tile else {})},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "parity": parity,

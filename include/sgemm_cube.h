@@ -258,9 +258,11 @@ int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t
  * Measurement hook for the tile-shape and k-depth sweep (Sec. 6.3 sweeps the
  * block sizes b_m, b_k, b_n of its pipeline): sgemm_cube_compute with the
  * elementwise order on a generic kernel with tile_m x tile_n tiles of C and
- * block_k of k per double-buffered LDS stage, one of
- *   (256, 256, 32), (256, 128, 32), (128, 256, 32), (128, 128, 32) with two
- *   workgroups per compute unit, (128, 128, 64).
+ * block_k of k per double-buffered LDS stage, computed by workgroups of
+ * `waves` waves, one of (tile_m, tile_n, block_k, waves) =
+ *   (256, 256, 32, 4), (256, 128, 32, 4), (128, 256, 32, 4), (128, 128, 32, 4)
+ *   with two workgroups per compute unit, (128, 128, 64, 4), and
+ *   (256, 256, 32, 8): two waves per SIMD, each wave 128 x 64 of the tile.
  * Every configuration applies the library's MFMA operations to each
  * accumulator in the same order, so all of them, and sgemm_cube_compute,
  * give identical results.  The generic kernel keeps one code shape for every
@@ -268,14 +270,14 @@ int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t
  * 16-column block, the next stage's copies spread over the first k-step);
  * the library's own 256 x 256 kernel is scheduled by hand and is faster.
  * accum_order other than SGEMM_CUBE_ELEMENTWISE ->
- * SGEMM_CUBE_ERR_NOT_SUPPORTED; another (tile_m, tile_n, block_k) ->
+ * SGEMM_CUBE_ERR_NOT_SUPPORTED; another (tile_m, tile_n, block_k, waves) ->
  * SGEMM_CUBE_ERR_INVALID_VALUE; otherwise as sgemm_cube_compute (scales
  * above 2^15, or a range flag that the split of B set, take the unscaled
  * fallback kernel as there).
  */
 int sgemm_cube_compute_tile(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
-                            int accum_order, int tile_m, int tile_n, int block_k, const void* ws,
-                            size_t ws_bytes, hipStream_t stream);
+                            int accum_order, int tile_m, int tile_n, int block_k, int waves,
+                            const void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Device workspace in bytes that sgemm_cube_ws needs for this problem
  * (0 for degenerate shapes); 0 also for invalid arguments. */

@@ -78,8 +78,8 @@ def _load() -> ctypes.CDLL:
         "sgemm_cube_splits_a_in_gemm": (i32, [i64, i64, i64, ptr, i64, f32, i32]),
         "sgemm_cube_compute_stages": (i32, [i64, i64, i64, ptr, i64, f32, i32, i32, ptr, sz,
                                             ptr]),
-        "sgemm_cube_compute_tile": (i32, [i64, i64, i64, ptr, i64, f32, i32, i32, i32, i32, ptr,
-                                          sz, ptr]),
+        "sgemm_cube_compute_tile": (i32, [i64, i64, i64, ptr, i64, f32, i32, i32, i32, i32, i32,
+                                          ptr, sz, ptr]),
         "sgemm_cube_workspace_size": (sz, [i64, i64, i64, i32]),
         "sgemm_cube_split": (i32, [i64, i64, ptr, i64, ptr, ptr, i64, f32, ptr]),
         "sgemm_cube_hgemm": (i32, [i64, i64, i64, ptr, i64, ptr, i64, ptr, i64, ptr]),
@@ -149,14 +149,15 @@ def sgemm_cube_compute_stages(M, N, K, C, ldc, scale, accum_order, stages, ws, w
                                           ws_bytes, stream)
 
 
-def sgemm_cube_compute_tile(M, N, K, C, ldc, scale, accum_order, tile_m, tile_n, block_k, ws,
-                            ws_bytes, stream) -> int:
+def sgemm_cube_compute_tile(M, N, K, C, ldc, scale, accum_order, tile_m, tile_n, block_k, waves,
+                            ws, ws_bytes, stream) -> int:
     return _lib.sgemm_cube_compute_tile(M, N, K, C, ldc, scale, accum_order, tile_m, tile_n,
-                                        block_k, ws, ws_bytes, stream)
+                                        block_k, waves, ws, ws_bytes, stream)
 
 
-# (tile_m, tile_n, block_k) configurations of sgemm_cube_compute_tile.
-TILE_CONFIGS = ((256, 256, 32), (256, 128, 32), (128, 256, 32), (128, 128, 32), (128, 128, 64))
+# (tile_m, tile_n, block_k, waves) configurations of sgemm_cube_compute_tile.
+TILE_CONFIGS = ((256, 256, 32, 4), (256, 128, 32, 4), (128, 256, 32, 4), (128, 128, 32, 4),
+                (128, 128, 64, 4), (256, 256, 32, 8))
 
 
 def sgemm_cube_workspace_size(M, N, K, accum_order=ELEMENTWISE) -> int:

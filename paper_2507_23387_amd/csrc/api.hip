@@ -289,13 +289,14 @@ int scratch_address(void** out) {
 // stages == 0 and tile_m == 0 mean the library's default kernels.
 int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale, int accum_order,
             int stages, const void* ws, size_t ws_bytes, hipStream_t stream, int tile_m = 0,
-            int tile_n = 0, int block_k = 0) {
+            int tile_n = 0, int block_k = 0, int waves = 0) {
   if (!valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (M < 0 || N < 0 || K < 0 || ldc < (N > 1 ? N : 1) || !valid_scale(scale))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   if (stages < 0 || stages > 2) return SGEMM_CUBE_ERR_INVALID_VALUE;
-  const bool tile = tile_m != 0 || tile_n != 0 || block_k != 0;
-  if (tile && !tile_config_ok(tile_m, tile_n, block_k)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const bool tile = tile_m != 0 || tile_n != 0 || block_k != 0 || waves != 0;
+  if (tile && !tile_config_ok(tile_m, tile_n, block_k, waves))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
   if ((stages != 0 || tile) && accum_order != SGEMM_CUBE_ELEMENTWISE)
     return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
@@ -310,7 +311,7 @@ int compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
   if (overlap(ws, need, C, span_bytes(M, N, ldc, 4))) return SGEMM_CUBE_ERR_INVALID_VALUE;
   const Planes p = plan_planes(M, N, K, const_cast<void*>(ws));
   const hipError_t e =
-      tile ? launch_gemm_tile(p, M, N, C, ldc, scale, tile_m, tile_n, block_k, stream)
+      tile ? launch_gemm_tile(p, M, N, C, ldc, scale, tile_m, tile_n, block_k, waves, stream)
       : stages == 0
           ? launch_gemm(p, M, N, C, ldc, scale, variant_of(accum_order), stream)
           : launch_gemm_stages(p, M, N, C, ldc, scale, stages, stream);
@@ -485,11 +486,12 @@ int sgemm_cube_compute_stages(int64_t M, int64_t N, int64_t K, float* C, int64_t
 }
 
 int sgemm_cube_compute_tile(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
-                            int accum_order, int tile_m, int tile_n, int block_k, const void* ws,
-                            size_t ws_bytes, hipStream_t stream) {
-  if (tile_m == 0 && tile_n == 0 && block_k == 0) return SGEMM_CUBE_ERR_INVALID_VALUE;
+                            int accum_order, int tile_m, int tile_n, int block_k, int waves,
+                            const void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (tile_m == 0 && tile_n == 0 && block_k == 0 && waves == 0)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
   return sgc::compute(M, N, K, C, ldc, scale, accum_order, 0, ws, ws_bytes, stream, tile_m,
-                      tile_n, block_k);
+                      tile_n, block_k, waves);
 }
 
 size_t sgemm_cube_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order) {

@@ -181,12 +181,12 @@ hipError_t launch_gemm_unscaled(const Planes& p, int64_t M, int64_t N, float* C,
 
 // The tile-shape and k-depth sweep of the scaled elementwise kernel
 // (gemm_tile.hip): tile_m x tile_n tiles of C with block_k of k per pipeline
-// stage, one of the configurations tile_config_ok accepts; the same bits as
-// launch_gemm's elementwise order.  Scales above 2^15 and a set range flag
-// take the unscaled kernel, as there.
-bool tile_config_ok(int tile_m, int tile_n, int block_k);
+// stage, computed by workgroups of `waves` waves, one of the configurations
+// tile_config_ok accepts; the same bits as launch_gemm's elementwise order.
+// Scales above 2^15 and a set range flag take the unscaled kernel, as there.
+bool tile_config_ok(int tile_m, int tile_n, int block_k, int waves);
 hipError_t launch_gemm_tile(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,
-                            float scale, int tile_m, int tile_n, int block_k,
+                            float scale, int tile_m, int tile_n, int block_k, int waves,
                             hipStream_t stream);
 
 // True when the order (kElementwise or kTermwise) can split A inside its GEMM

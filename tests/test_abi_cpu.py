@@ -191,15 +191,17 @@ def test_compute_stages_validation(lib):
 
 def test_compute_tile_validation(lib):
     ws = FAKE + (3 << 30)
-    call = lambda order=0, tm=256, tn=256, bk=32, M=4: lib.sgemm_cube_compute_tile(
-        M, 4, 4, FAKE, 4, 2048.0, order, tm, tn, bk, ws, 1 << 20, 0)
-    assert call(tm=0, tn=0, bk=0) == INVALID
-    for cfg in ((64, 64, 32), (256, 256, 64), (256, 128, 64), (128, 128, 16), (384, 128, 32)):
-        assert call(tm=cfg[0], tn=cfg[1], bk=cfg[2]) == INVALID, cfg
+    call = lambda order=0, tm=256, tn=256, bk=32, w=4, M=4: lib.sgemm_cube_compute_tile(
+        M, 4, 4, FAKE, 4, 2048.0, order, tm, tn, bk, w, ws, 1 << 20, 0)
+    assert call(tm=0, tn=0, bk=0, w=0) == INVALID
+    for cfg in ((64, 64, 32, 4), (256, 256, 64, 4), (256, 128, 64, 4), (128, 128, 16, 4),
+                (384, 128, 32, 4), (256, 256, 32, 0), (256, 256, 32, 2), (256, 256, 32, 16),
+                (256, 128, 32, 8), (128, 128, 32, 8), (0, 0, 0, 8)):
+        assert call(tm=cfg[0], tn=cfg[1], bk=cfg[2], w=cfg[3]) == INVALID, cfg
     assert call(order=1) == NOT_SUPPORTED
     assert call(order=3) == INVALID
     for cfg in lib.TILE_CONFIGS:
-        assert call(M=0, tm=cfg[0], tn=cfg[1], bk=cfg[2]) == 0   # validation only
+        assert call(M=0, tm=cfg[0], tn=cfg[1], bk=cfg[2], w=cfg[3]) == 0   # validation only
 
 
 def test_compute_a_validation(lib):

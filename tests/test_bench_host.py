@@ -123,3 +123,24 @@ def test_hi_only_gap():
     assert bench.hi_only_gap(o, o, h) == 0.0
     assert bench.hi_only_gap(o + np.float32(0.25), o, h) == 0.5
     assert bench.hi_only_gap(o, o, o) is None
+
+
+def test_tile_keys_name_the_sweep_kernels():
+    from paper_2507_23387_amd import binding
+
+    names = set()
+    for tile in binding.TILE_CONFIGS:
+        key = "elementwise_tile_" + bench.tile_name(tile)
+        name = bench.gemm_kernel_name(key)
+        assert name.startswith(f"gemm_tile_kernel<{tile[0]}, {tile[1]}, {tile[2]}, ")
+        names.add(name)
+    assert len(names) == len(binding.TILE_CONFIGS)
+    # Four-wave keys keep the three-field form the committed profiles use.
+    assert bench.tile_name((256, 256, 32, 4)) == "256x256x32"
+    assert bench.gemm_kernel_name("elementwise_tile_256x256x32") == \
+        "gemm_tile_kernel<256, 256, 32, 1, 2, 2>"
+    assert bench.gemm_kernel_name("elementwise_tile_128x128x32") == \
+        "gemm_tile_kernel<128, 128, 32, 2, 2, 2>"
+    assert bench.tile_name((256, 256, 32, 8)) == "256x256x32x8"
+    assert bench.gemm_kernel_name("elementwise_tile_256x256x32x8") == \
+        "gemm_tile_kernel<256, 256, 32, 1, 2, 4>"
