@@ -48,13 +48,16 @@ HBM_PEAK_GBS = 8000.0
 # the unscaled 256 x 128 kernel, which reads the range flag and returns at once
 # unless some |B_hi| s exceeds 65504, in which case it does the work.  For
 # termwise the 256 x 128 kernel, likewise with A split in registers where the
-# library chooses it.
+# library chooses it, and with --split-b-in-gemm the same kernel splitting B
+# (and A, where the library splits A in the GEMM) itself.
 GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true, true>",
                 "elementwise_unfused": "gemm_el_kernel<true, false>",
-                "elementwise_unscaled": "gemm_n128_kernel<0, false>",
-                "termwise": "gemm_n128_kernel<1, false>",
-                "termwise_fused": "gemm_n128_kernel<1, true>",
-                "elementwise_cross_first": "gemm_n128_kernel<3, false>"}
+                "elementwise_unscaled": "gemm_n128_kernel<0, false, false>",
+                "termwise": "gemm_n128_kernel<1, false, false>",
+                "termwise_fused": "gemm_n128_kernel<1, true, false>",
+                "termwise_fused_b": "gemm_n128_kernel<1, false, true>",
+                "termwise_fused_ab": "gemm_n128_kernel<1, true, true>",
+                "elementwise_cross_first": "gemm_n128_kernel<3, false, false>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
@@ -315,6 +318,10 @@ def main():
     ap.add_argument("--unfused", action="store_true",
                     help="split A into the workspace and run the GEMM on the A planes also where "
                          "sgemm_cube would split A inside the GEMM kernel")
+    ap.add_argument("--split-b-in-gemm", action="store_true",
+                    help="termwise only: split B inside the GEMM kernel (sgemm_cube_compute_b "
+                         "after a split pass of A, or one sgemm_cube_ex call with "
+                         "SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM where A is split in the GEMM too)")
     ap.add_argument("--prescale", action="store_true",
                     help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -371,6 +378,11 @@ def main():
     fused = (not args.unfused and not args.stages and not args.prescale and not tile and
              sgc.binding.sgemm_cube_splits_a_in_gemm(M, N, K, dA.data_ptr(), K, scale,
                                                      order_code) == 1)
+    split_b = args.split_b_in_gemm
+    if split_b and (order != "termwise" or args.prescale or args.stages or tile):
+        print("--split-b-in-gemm: the termwise order only, without --prescale, --stages or "
+              "--tile", file=sys.stderr)
+        sys.exit(2)
 
     def prepare():
         st = sgc.sgemm_cube_prepare(M, N, K, None if fused else dA.data_ptr(), K, dB.data_ptr(),
@@ -394,6 +406,32 @@ def main():
                                         ws.data_ptr(), ws_bytes, sh)
         if st:
             raise sgc.SgemmCubeError(st, "sgemm_cube_compute")
+
+    if split_b and fused:
+        # Both operands split inside the GEMM kernel: one call, one kernel,
+        # timed in the "compute" slot.
+        def prepare():
+            pass
+
+        def compute():
+            st = sgc.sgemm_cube_ex(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, dC.data_ptr(), N,
+                                   scale, order_code, sgc.binding.OPT_SPLIT_B_IN_GEMM,
+                                   ws.data_ptr(), ws_bytes, None, sh)
+            if st:
+                raise sgc.SgemmCubeError(st, "sgemm_cube_ex")
+    elif split_b:
+        # The split pass of A, then the GEMM that splits B itself.
+        def prepare():
+            st = sgc.sgemm_cube_prepare(M, N, K, dA.data_ptr(), K, None, N, scale, ws.data_ptr(),
+                                        ws_bytes, sh)
+            if st:
+                raise sgc.SgemmCubeError(st, "sgemm_cube_prepare")
+
+        def compute():
+            st = sgc.binding.sgemm_cube_compute_b(M, N, K, dB.data_ptr(), N, dC.data_ptr(), N,
+                                                  scale, order_code, ws.data_ptr(), ws_bytes, sh)
+            if st:
+                raise sgc.SgemmCubeError(st, "sgemm_cube_compute_b")
 
     if args.prescale:
         # The pre-scaled call has no split/compute halves: the whole call is
@@ -472,6 +510,8 @@ def main():
             kernel_key = "elementwise_tile_" + tile_name(tile)
         elif not fused:
             kernel_key = "elementwise_unfused"
+    elif order == "termwise" and split_b:
+        kernel_key = "termwise_fused_ab" if fused else "termwise_fused_b"
     elif order == "termwise" and fused:
         kernel_key = "termwise_fused"
     traffic = traffic_entry(w.name, kernel_key)
@@ -487,13 +527,13 @@ def main():
         "avg_launch_ms": gemm_ms,
     }
     # 4 B read + 2 x 2 B written per element split (B only when A is split in
-    # the GEMM kernel).
-    split_bytes = 8.0 * ((0 if fused else M * K) + K * N)
+    # the GEMM kernel, A only when B is).
+    split_bytes = 8.0 * ((0 if fused else M * K) + (0 if split_b else K * N))
     extra = {
         "pct_of_3gemm_peak": 100 * value / THREE_GEMM_PEAK_TFLOPS,
         "three_gemm_peak_tflops": THREE_GEMM_PEAK_TFLOPS,
         "split_ms": split_ms,
-        "split_gbs": split_bytes / (split_ms * 1e-3) / 1e9,
+        "split_gbs": split_bytes / (split_ms * 1e-3) / 1e9 if split_bytes else None,
         "device_copy_gbs": copy_gbs,
         "gemm_ms": gemm_ms,
         "step_ms": {"median": float(np.median(step_times)), "min": float(step_times.min()),
@@ -581,6 +621,7 @@ def main():
                    "distribution": w.dist, "scale": scale, "order": order,
                    **({"prescale": True} if args.prescale else {}),
                    "split_of_a": "in the GEMM kernel" if fused else "separate pass",
+                   "split_of_b": "in the GEMM kernel" if split_b else "separate pass",
                    **({"stages": args.stages} if args.stages else {}),
                    **({"tile": tile_name(tile)} if tile else {})},
         "roofline": roofline,

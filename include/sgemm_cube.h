@@ -132,7 +132,7 @@ int sgemm_cube_noalloc(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
                        int accum_order, hipStream_t stream);
 
 /* Options of sgemm_cube_ex (bit mask). */
-enum { SGEMM_CUBE_OPT_PRESCALE = 1 };
+enum { SGEMM_CUBE_OPT_PRESCALE = 1, SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM = 2 };
 
 /* Range classes reported by sgemm_cube_ex (bit mask; Sec. 3.1 and 4.2). */
 enum {
@@ -148,7 +148,8 @@ enum {
  * and Sec. 7 and 8 name as the way to widen the method's range (explicit
  * exponent management of the high part, input-dependent scaling, an overflow
  * guard):
- *   options      0 or SGEMM_CUBE_OPT_PRESCALE.  With PRESCALE, row i of A is
+ *   options      0, SGEMM_CUBE_OPT_PRESCALE or SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM.
+ *                With PRESCALE, row i of A is
  *                multiplied by 2^p_i and column j of B by 2^q_j before the
  *                split, powers of two that bring the row's (column's) largest
  *                finite magnitude into [2^EA, 2^(EA+1)) with
@@ -161,6 +162,18 @@ enum {
  *                of their row's (column's) largest entry.  A row (column) with
  *                no nonzero finite entry is left unscaled.  Costs one extra
  *                read of A and B and one read-write of C.
+ *                With SPLIT_B_IN_GEMM (the fused split of Sec. 3.3 applied to
+ *                B as well as A), the termwise GEMM kernel reads B as FP32 and
+ *                splits it itself, each B tile once per tile row of C, instead
+ *                of a split pass writing B's planes; A is split inside the
+ *                kernel too where sgemm_cube_splits_a_in_gemm says so, so then
+ *                no plane reaches HBM.  The result is that of the termwise
+ *                order without the option, bit for bit.  Requires
+ *                accum_order = SGEMM_CUBE_TERMWISE, no PRESCALE, range_report
+ *                NULL, B 16-byte aligned, ldb and N multiples of 4, K a
+ *                multiple of 64 and ldb < 2^22; otherwise
+ *                SGEMM_CUBE_ERR_NOT_SUPPORTED.  The workspace is that of the
+ *                call without the option.
  *   range_report NULL, or a 4-byte-aligned DEVICE pointer to one uint32 that
  *                receives, in stream order, the OR of the SGEMM_CUBE_RANGE_*
  *                classes found among the (pre-scaled) entries of A and B; 0 when
@@ -217,6 +230,24 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
  * same M, N, K and scale as the prepare of B (the library cannot check this).
  * Afterwards the workspace's A planes are unspecified.
  */
+/*
+ * The mirror image for a workspace whose A planes are prepared
+ * (sgemm_cube_prepare with B == NULL), termwise order only: the GEMM kernel
+ * reads B as FP32 and splits it itself (Sec. 3.3: the fused split, applied to
+ * B; each B tile is split once per tile row of C), so B's planes are never
+ * written.  Gives the same bits as sgemm_cube_ws(...) with the termwise
+ * order.  Useful when one A multiplies many B.
+ * accum_order other than SGEMM_CUBE_TERMWISE, or B not 16-byte aligned, ldb
+ * or N not a multiple of 4, K not a multiple of 64, or ldb >= 2^22 ->
+ * SGEMM_CUBE_ERR_NOT_SUPPORTED.  M, N, K, B, ldb, C, ldc, scale, ws,
+ * ws_bytes and the other errors follow sgemm_cube_ws; C must not overlap B
+ * or the workspace.  Must use the same M, N, K and scale as the prepare of A
+ * (the library cannot check this).
+ */
+int sgemm_cube_compute_b(int64_t M, int64_t N, int64_t K, const float* B, int64_t ldb,
+                         float* C, int64_t ldc, float scale, int accum_order, const void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
 int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
                          float* C, int64_t ldc, float scale, int accum_order, void* ws,
                          size_t ws_bytes, hipStream_t stream);

@@ -25,6 +25,7 @@ _EXPORTS = (
     "sgemm_cube_block_k",
     "sgemm_cube_compute",
     "sgemm_cube_compute_a",
+    "sgemm_cube_compute_b",
     "sgemm_cube_compute_stages",
     "sgemm_cube_compute_tile",
     "sgemm_cube_ex",

@@ -23,6 +23,7 @@ ORDERS = {"elementwise": ELEMENTWISE, "termwise": TERMWISE,
           "elementwise_cross_first": ELEMENTWISE_CROSS_FIRST}
 
 OPT_PRESCALE = 1
+OPT_SPLIT_B_IN_GEMM = 2
 RANGE_NONFINITE = 1
 RANGE_HI_OVERFLOW = 2
 RANGE_LO_OVERFLOW = 4
@@ -40,7 +41,7 @@ STATUS_NAMES = {
 # Every symbol include/sgemm_cube.h declares.
 EXPORTS = (
     "sgemm_cube", "sgemm_cube_ws", "sgemm_cube_noalloc", "sgemm_cube_ex", "sgemm_cube_ex_workspace_size",
-    "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_a",
+    "sgemm_cube_prepare", "sgemm_cube_compute", "sgemm_cube_compute_a", "sgemm_cube_compute_b",
     "sgemm_cube_splits_a_in_gemm", "sgemm_cube_compute_stages", "sgemm_cube_compute_tile",
     "sgemm_cube_workspace_size", "sgemm_cube_split",
     "sgemm_cube_hgemm", "sgemm_cube_status_string",
@@ -74,6 +75,8 @@ def _load() -> ctypes.CDLL:
         "sgemm_cube_prepare": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, ptr, sz, ptr]),
         "sgemm_cube_compute": (i32, [i64, i64, i64, ptr, i64, f32, i32, ptr, sz, ptr]),
         "sgemm_cube_compute_a": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, i32, ptr, sz,
+                                       ptr]),
+        "sgemm_cube_compute_b": (i32, [i64, i64, i64, ptr, i64, ptr, i64, f32, i32, ptr, sz,
                                        ptr]),
         "sgemm_cube_splits_a_in_gemm": (i32, [i64, i64, i64, ptr, i64, f32, i32]),
         "sgemm_cube_compute_stages": (i32, [i64, i64, i64, ptr, i64, f32, i32, i32, ptr, sz,
@@ -136,6 +139,12 @@ def sgemm_cube_compute(M, N, K, C, ldc, scale, accum_order, ws, ws_bytes, stream
 def sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes,
                          stream) -> int:
     return _lib.sgemm_cube_compute_a(M, N, K, A, lda, C, ldc, scale, accum_order, ws, ws_bytes,
+                                     stream)
+
+
+def sgemm_cube_compute_b(M, N, K, B, ldb, C, ldc, scale, accum_order, ws, ws_bytes,
+                         stream) -> int:
+    return _lib.sgemm_cube_compute_b(M, N, K, B, ldb, C, ldc, scale, accum_order, ws, ws_bytes,
                                      stream)
 
 

@@ -117,6 +117,9 @@ size_t ws_size(int64_t M, int64_t N, int64_t K, bool prescale = false) {
   return plan_planes(M, N, K, nullptr, prescale).bytes;
 }
 
+// Option bits sgemm_cube_ex accepts.
+constexpr unsigned kExOptions = SGEMM_CUBE_OPT_PRESCALE | SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM;
+
 // Target exponents of the pre-scaled row (A) and column (B) maxima for
 // s = 2^s_b: [2^EA, 2^(EA+1)) with EA = min(14, 26 - s_b) keeps hi finite and
 // the scaled residual of every entry below 2^16 (Rule 2, Sec. 4.2); B's
@@ -170,7 +173,8 @@ hipError_t compute_from_a(const Planes& p, int64_t M, int64_t N, int64_t K, cons
 // not null, receives the range classes (device word).
 int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const float* B,
         int64_t ldb, float* C, int64_t ldc, float scale, int variant, void* ws,
-        hipStream_t stream, const RangeOpts& opt = RangeOpts{}, uint32_t* report = nullptr) {
+        hipStream_t stream, const RangeOpts& opt = RangeOpts{}, uint32_t* report = nullptr,
+        bool split_b_in_gemm = false) {
   if (M == 0 || N == 0 || K == 0) {
     if (M > 0 && N > 0 && launch_zero(M, N, C, ldc, stream) != hipSuccess)
       return SGEMM_CUBE_ERR_HIP;
@@ -179,6 +183,18 @@ int run(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, const floa
     return SGEMM_CUBE_OK;
   }
   const Planes p = plan_planes(M, N, K, ws, opt.prescale);
+  if (split_b_in_gemm) {
+    // Termwise with B split inside the GEMM kernel (validated by the caller);
+    // A too where the library splits it there, else by its own pass.
+    const bool fused_a = splits_a_in_gemm(N, A, lda, K, scale, variant);
+    if (!fused_a &&
+        launch_split_a(p, M, K, A, lda, scale, opt, next_stamp(), stream) != hipSuccess)
+      return SGEMM_CUBE_ERR_HIP;
+    return launch_gemm_fused_b(p, M, N, K, A, lda, fused_a, B, ldb, C, ldc, scale, stream) ==
+                   hipSuccess
+               ? SGEMM_CUBE_OK
+               : SGEMM_CUBE_ERR_HIP;
+  }
   if (!opt.prescale && !opt.report && splits_a_in_gemm(N, A, lda, K, scale, variant)) {
     // B is split into the workspace, A inside the GEMM kernel.
     if (launch_split_b(p, K, N, B, ldb, scale, opt, next_stamp(), stream) != hipSuccess)
@@ -374,11 +390,15 @@ int sgemm_cube_ex(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
                   int64_t ldb, float* C, int64_t ldc, float scale, int accum_order,
                   unsigned options, void* ws, size_t ws_bytes, uint32_t* range_report,
                   hipStream_t stream) {
-  if (!sgc::valid_order(accum_order) || (options & ~static_cast<unsigned>(SGEMM_CUBE_OPT_PRESCALE)))
+  if (!sgc::valid_order(accum_order) || (options & ~sgc::kExOptions))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   int st = sgc::validate_gemm(M, N, K, A, lda, B, ldb, C, ldc, scale, true);
   if (st != SGEMM_CUBE_OK) return st;
   const bool prescale = (options & SGEMM_CUBE_OPT_PRESCALE) != 0;
+  const bool split_b = (options & SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM) != 0;
+  if (split_b && (accum_order != SGEMM_CUBE_TERMWISE || prescale || range_report ||
+                  !sgc::fused_split_b_ok(B, ldb, N, K)))
+    return SGEMM_CUBE_ERR_NOT_SUPPORTED;
   const size_t need = sgc::ws_size(M, N, K, prescale);
   if (ws_bytes < need || (need > 0 && (!ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
@@ -394,13 +414,13 @@ int sgemm_cube_ex(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda, 
                        sgc::overlap(range_report, 4, ws, need)))
     return SGEMM_CUBE_ERR_INVALID_VALUE;
   return sgc::run(M, N, K, A, lda, B, ldb, C, ldc, scale, sgc::variant_of(accum_order), ws,
-                  stream, sgc::range_opts(options, range_report != nullptr, scale), range_report);
+                  stream, sgc::range_opts(options, range_report != nullptr, scale), range_report,
+                  split_b);
 }
 
 size_t sgemm_cube_ex_workspace_size(int64_t M, int64_t N, int64_t K, int accum_order,
                                     unsigned options) {
-  if (!sgc::valid_order(accum_order) || (options & ~static_cast<unsigned>(SGEMM_CUBE_OPT_PRESCALE)))
-    return 0;
+  if (!sgc::valid_order(accum_order) || (options & ~sgc::kExOptions)) return 0;
   if (M < 0 || N < 0 || K < 0 || M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim)
     return 0;
   return sgc::ws_size(M, N, K, (options & SGEMM_CUBE_OPT_PRESCALE) != 0);
@@ -436,6 +456,37 @@ int sgemm_cube_prepare(int64_t M, int64_t N, int64_t K, const float* A, int64_t 
 int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, float scale,
                        int accum_order, const void* ws, size_t ws_bytes, hipStream_t stream) {
   return sgc::compute(M, N, K, C, ldc, scale, accum_order, 0, ws, ws_bytes, stream);
+}
+
+int sgemm_cube_compute_b(int64_t M, int64_t N, int64_t K, const float* B, int64_t ldb,
+                         float* C, int64_t ldc, float scale, int accum_order, const void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  if (!sgc::valid_order(accum_order)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M < 0 || N < 0 || K < 0 || ldb < (N > 1 ? N : 1) || ldc < (N > 1 ? N : 1) ||
+      !sgc::valid_scale(scale))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if ((K > 0 && N > 0 && !B) || (M > 0 && N > 0 && !C)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (!sgc::ld_ok(K, ldb) || !sgc::ld_ok(M, ldc)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (M > sgc::kMaxDim || N > sgc::kMaxDim || K > sgc::kMaxDim) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (sgc::round_up_tiles_exceed(M, N)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  const uint64_t bb = sgc::span_bytes(K, N, ldb, 4), cb = sgc::span_bytes(M, N, ldc, 4);
+  if (sgc::overlap(C, cb, B, bb)) return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (accum_order != SGEMM_CUBE_TERMWISE) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  if (M == 0 || N == 0) return SGEMM_CUBE_OK;
+  if (K == 0)
+    return sgc::launch_zero(M, N, C, ldc, stream) == hipSuccess ? SGEMM_CUBE_OK
+                                                                : SGEMM_CUBE_ERR_HIP;
+  if (!sgc::fused_split_b_ok(B, ldb, N, K)) return SGEMM_CUBE_ERR_NOT_SUPPORTED;
+  const size_t need = sgc::ws_size(M, N, K);
+  if (ws_bytes < need || !ws || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  if (sgc::overlap(ws, need, B, bb) || sgc::overlap(ws, need, C, cb))
+    return SGEMM_CUBE_ERR_INVALID_VALUE;
+  const sgc::Planes p = sgc::plan_planes(M, N, K, const_cast<void*>(ws));
+  return sgc::launch_gemm_fused_b(p, M, N, K, nullptr, 0, false, B, ldb, C, ldc, scale,
+                                  stream) == hipSuccess
+             ? SGEMM_CUBE_OK
+             : SGEMM_CUBE_ERR_HIP;
 }
 
 int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,

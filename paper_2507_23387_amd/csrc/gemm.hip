@@ -16,7 +16,9 @@
 //                    that need three accumulator sets -- termwise (Eq.
 //                    termwise), the unscaled elementwise fallback (range
 //                    flag set) and the cross-terms-first order (end of
-//                    Sec. 4.5).
+//                    Sec. 4.5); termwise also on FP32 A split in registers
+//                    (kFusedA) and on FP32 B that the workgroup splits into
+//                    its LDS planes (kFusedB).
 //   gemm_hi_kernel   256 x 256 tiles: HH only, the native-FP16 baseline.
 // The tile-shape sweep of the scaled elementwise order is in gemm_tile.hip.
 // For the elementwise order with s <= 2^15 both elementwise kernels are
@@ -567,11 +569,27 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // vector instructions of the split, one between consecutive MFMAs (two once),
 // into the register set of step kt+1.  The last of them comes 10 MFMAs
 // before that set's first use.  The bits are those of the planes path.
+//
+// kFusedB (termwise only; with or without kFusedA): no B planes are read.
+// Two more LDS slots (16 KiB each, 128 KiB in all) hold the FP32 rows of B
+// for the stage, 32 k-rows x 128 columns, copied verbatim by LDS DMA one
+// stage ahead as A is (columns past N repeat the last four; N is a multiple
+// of 4 here).  The workgroup splits them into the B plane slots itself (Sec.
+// 3.3): during blocks 2-6 of step kt, each thread splits one column, k
+// 16 (t / 128) .. + 15 of stage kt+1, reading its 16 values from the FP32
+// slot (each read has the 64 lanes of a wave on 64 consecutive words) and
+// writing the high and the scaled residual words as the 16-byte chunks of
+// the tiled plane layout, so everything after that is the planes path: the
+// same fragments, the same MFMAs, the same bits.  The barrier before block 7,
+// which publishes B stage kt+1, also publishes these writes; the FP32 slot
+// is refilled (stage kt+3) only after it.
 constexpr int kTwM = 256;
 constexpr int kTwN = 128;
 constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
 constexpr int kTwBSlot = 2 * kTwN * kStep;        // halves: B_hi, B_lo of one step
+constexpr int kTwBfSlotBytes = kTwN * kStep * 4;  // FP32 B rows of one step: 16 KiB
 constexpr size_t kTwLdsBytes = static_cast<size_t>(2) * (kTwASlot + kTwBSlot) * 2;  // 96 KiB
+constexpr size_t kTwFusedBLdsBytes = kTwLdsBytes + 2 * kTwBfSlotBytes;             // 128 KiB
 
 // Slot (the MFMA of a step, 12 per column block, after which it is issued)
 // of split instruction q (0-79: 16-row block q / 20, instruction q % 20) in
@@ -584,15 +602,17 @@ constexpr int tw_split_slot(int q) {
   return kTwSplitFirst + q * (kTwSplitLast - kTwSplitFirst + 1) / 80;
 }
 
-template <int V, bool kFusedA = false>
+template <int V, bool kFusedA = false, bool kFusedB = false>
 __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     const uint16_t* __restrict__ a_hi, const uint16_t* __restrict__ a_lo,
     const uint16_t* __restrict__ b_hi, const uint16_t* __restrict__ b_lo,
     const uint32_t* __restrict__ range, int Kp, int tiles_m, int tiles_n,
     float* __restrict__ C, int64_t ldc, int M, int N, float inv_s, int unscaled_only,
-    const float* __restrict__ af, int64_t lda, float s) {
+    const float* __restrict__ af, int64_t lda, float s, const float* __restrict__ bf,
+    int64_t ldb) {
   static_assert(V == kTermwise || V == kElementwise || V == kCrossFirst, "n128 variants");
   static_assert(!kFusedA || V == kTermwise, "the fused split of A is built for termwise only");
+  static_assert(!kFusedB || V == kTermwise, "the fused split of B is built for termwise only");
   constexpr bool kFold = V != kTermwise;
   constexpr int kRows = 4;                   // 16-row blocks per wave
   constexpr int kCols = 8;                   // 16-column blocks per wave
@@ -603,6 +623,12 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
                     static_cast<size_t>(kBBase) * 2, "A DMAs stay in the A slots");
   static_assert(dma_end_bytes(kBBase + kTwBSlot + kBPlane + kTileHalves) <= kTwLdsBytes &&
                     kTwLdsBytes <= kMaxLdsBytes, "B DMAs stay in LDS");
+  // Fused split of B: the FP32 slots follow the B plane slots; DMA d (0-3) of
+  // wave w fills 1 KiB block w + 4 d of a slot.
+  constexpr int kBfBase = 2 * kBBase + 2 * kTwBSlot * 2;  // bytes
+  static_assert(kBfBase == static_cast<int>(kTwLdsBytes), "FP32 B slots follow the planes");
+  static_assert(kBfBase + kTwBfSlotBytes + 3 * 4096 + 4096 <= static_cast<int>(kTwFusedBLdsBytes) &&
+                    kTwFusedBLdsBytes <= kMaxLdsBytes, "FP32 B DMAs stay in LDS");
   if constexpr (V == kElementwise) {
     // Unless the host routed the call here (unscaled_only: s is not a finite
     // FP16 value), the scaled 256 x 256 kernel handles the case where the
@@ -661,11 +687,35 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     dma16s(a_tile + static_cast<int64_t>(tc) * kStep, a_voff[d],
            lds_base + (t & 1) * kTwASlot * 2 + d * 4096);
   };
-  // The d-th of the 12 DMAs of step kt: B stage kt+1, then A stage kt+2.
+  // Fused split of B: lane l of DMA d of wave w copies k-row
+  // 2 (w + 4 d) + l / 32 of the stage, columns 4 (l % 32) .. + 3 of the tile
+  // (clamped to the last four columns of B), to byte 512 k-row + 16 (l % 32)
+  // of the slot.  K is a multiple of 64 here, so no copy reads past row K - 1.
+  unsigned b_voff[kFusedB ? 4 : 1];
+  const float* b_tile = nullptr;
+  if constexpr (kFusedB) {
+    const int col = min(tn * kTwN + 4 * (lane & 31), N - 4);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const int row = 2 * (w + 4 * d) + (lane >> 5);
+      b_voff[d] = static_cast<unsigned>((row * ldb + col) * 4);
+    }
+    b_tile = bf;
+  }
+  auto dma_bf = [&](int t, int d) {
+    const int tc = min(t, ksteps - 1);
+    dma16s(b_tile + static_cast<int64_t>(tc) * kStep * ldb, b_voff[d],
+           lds_base + kBfBase + (t & 1) * kTwBfSlotBytes + d * 4096);
+  };
+  // The d-th of the 12 DMAs of step kt: B stage kt+1 (FP32 B: stage kt+2),
+  // then A stage kt+2.
   auto dma = [&](int kt, int d) {
-    if (d < 4)
-      dma_b(kt + 1, d);
-    else if constexpr (kFusedA)
+    if (d < 4) {
+      if constexpr (kFusedB)
+        dma_bf(kt + 2, d);
+      else
+        dma_b(kt + 1, d);
+    } else if constexpr (kFusedA)
       dma_af(kt + 2, d - 4);
     else
       dma_a(kt + 2, d - 4);
@@ -726,6 +776,37 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     }
   };
 
+  // Fused split of B: thread t splits column bn = t % 128 of the tile, k
+  // 16 bs .. 16 bs + 15 of a stage (bs = t / 128: slice bs of the stage),
+  // as two chunks of eight k.  Chunk ch: bsplit_read loads its eight FP32
+  // values from the stage's FP32 slot (k-row r at byte 512 r, column bn at
+  // 4 bn; the 64 lanes of a wave read 64 consecutive words), bsplit_op<q> is
+  // instruction q (0-19) of their split (pair q / 5, step q % 5 of
+  // split_op), and bsplit_write stores the four high words and the four
+  // scaled residual words as chunk ch of row bn of the slice's plane tiles,
+  // at chunk position ch ^ tile_swizzle(bn), as the split kernel of B lays
+  // them out.
+  const int bn = threadIdx.x & (kTwN - 1), bs = threadIdx.x >> 7;
+  float bfv[8], brr[2];
+  uint32_t bhw[4], blw[4];
+  auto bsplit_read = [&](int t, int ch) {
+    const float* src = reinterpret_cast<const float*>(reinterpret_cast<const char*>(lds) +
+                                                      kBfBase + (t & 1) * kTwBfSlotBytes);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) bfv[e] = src[(16 * bs + 8 * ch + e) * kTwN + bn];
+  };
+  auto bsplit_op = [&](auto Qc) {
+    constexpr int q = decltype(Qc)::value, pr = q / 5, op = q % 5;
+    split_op<op>(bhw[pr], blw[pr], brr, bfv[2 * pr], bfv[2 * pr + 1], s_sgpr);
+  };
+  auto bsplit_write = [&](int t, int ch) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const int off = kBBase + (t & 1) * kTwBSlot + bs * kTileHalves + bn * kSlice +
+                    ((ch ^ tile_swizzle(bn)) << 3);
+    *reinterpret_cast<u32x4*>(lds + off) = u32x4{bhw[0], bhw[1], bhw[2], bhw[3]};
+    *reinterpret_cast<u32x4*>(lds + off + kBPlane) = u32x4{blw[0], blw[1], blw[2], blw[3]};
+  };
+
   // Termwise: hh, xa, xb.  Block folds: acc (= hh) and the block sums t1, t2
   // of the current and the previous column block (index: block parity).
   floatx4 hh[kRows][kCols], xa[kFold ? 1 : kRows][kFold ? 1 : kCols],
@@ -750,7 +831,21 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     static_for<8>([&](auto n) { dma_a(0, decltype(n)::value); });
     static_for<8>([&](auto n) { dma_a(1, decltype(n)::value); });
   }
-  static_for<4>([&](auto n) { dma_b(0, decltype(n)::value); });
+  if constexpr (kFusedB) {
+    // FP32 B stages 0 and 1; stage 0 is split here, stage 1 during step 0.
+    static_for<4>([&](auto n) { dma_bf(0, decltype(n)::value); });
+    static_for<4>([&](auto n) { dma_bf(1, decltype(n)::value); });
+    wait_vmcnt<0>();
+    lds_barrier();
+#pragma unroll
+    for (int ch = 0; ch < 2; ++ch) {
+      bsplit_read(0, ch);
+      static_for<20>([&](auto q) { bsplit_op(q); });
+      bsplit_write(0, ch);
+    }
+  } else {
+    static_for<4>([&](auto n) { dma_b(0, decltype(n)::value); });
+  }
   wait_vmcnt<0>();
   lds_barrier();
   half8 AH[kRows], AL[kRows], NH[kRows], NL[kRows], bh[2], bl[2];
@@ -831,7 +926,10 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
         lds_barrier();
       }
       if constexpr (j == kCols - 1) {
-        wait_vmcnt<kADmas>();  // all but this step's A DMAs: B stage kt+1 is in
+        // All but this step's A DMAs: B stage kt+1 is in.  With the fused
+        // split of B the barrier publishes the split's writes of that stage
+        // instead, and every DMA of the step is for stage kt+2.
+        if constexpr (!kFusedB) wait_vmcnt<kADmas>();
         lds_barrier();
         bh[c ^ 1] = rd_b(kt + 1, 0, 0);
         bl[c ^ 1] = rd_b(kt + 1, 1, 0);
@@ -929,6 +1027,24 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
               nl[r - kRows] = rd_a(kt + 1, 1, r - kRows);
           }
         }
+        if constexpr (kFusedB) {
+          // Split of B stage kt+1 (landed at the barrier of block
+          // kAWaitBlock <= 2) into its plane slot, in slots 24-81 (blocks
+          // 2-6): chunk ch reads at slot 24 + 29 ch, issues one instruction
+          // per slot from eight slots later (the reads' latency, so the
+          // wave does not stall on them), and writes after the last.
+          constexpr int P = kRows * 3 * j + m;
+          static_assert(kRows * 3 * 2 >= kRows * 3 * kAWaitBlock &&
+                            kRows * 3 * 2 + 29 + 28 < kRows * 3 * (kCols - 1),
+                        "the split of B runs between the barriers of blocks 2 and 7");
+          static_for<2>([&](auto Ch) {
+            constexpr int ch = decltype(Ch)::value, P0 = kRows * 3 * 2 + 29 * ch;
+            if constexpr (P == P0) bsplit_read(kt + 1, ch);
+            if constexpr (P >= P0 + 8 && P < P0 + 28)
+              bsplit_op(std::integral_constant<int, P - P0 - 8>{});
+            if constexpr (P == P0 + 28) bsplit_write(kt + 1, ch);
+          });
+        }
         if constexpr (j < 4 && m % 4 == 2) dma(kt, kDmaPerBlock * j + m / 4);
         SCHED_FENCE();
       });
@@ -991,20 +1107,22 @@ hipError_t launch_hi(const Planes& p, int64_t M, int64_t N, float* C, int64_t ld
   return hipGetLastError();
 }
 
-template <int V, bool kFusedA = false>
+template <int V, bool kFusedA = false, bool kFusedB = false>
 hipError_t launch_n128(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc, float s,
                        hipStream_t stream, bool unscaled_only = false,
-                       const float* A = nullptr, int64_t lda = 0) {
+                       const float* A = nullptr, int64_t lda = 0, const float* B = nullptr,
+                       int64_t ldb = 0) {
+  constexpr size_t kLds = kFusedB ? kTwFusedBLdsBytes : kTwLdsBytes;
   static std::atomic<bool> done[kMaxDevices];
-  const hipError_t attr = set_lds(&gemm_n128_kernel<V, kFusedA>, kTwLdsBytes, done);
+  const hipError_t attr = set_lds(&gemm_n128_kernel<V, kFusedA, kFusedB>, kLds, done);
   if (attr != hipSuccess) return attr;
   const int tiles_m = static_cast<int>(p.Mp / kTwM);
   const int tiles_n = static_cast<int>(p.Np / kTwN);
-  hipLaunchKernelGGL((gemm_n128_kernel<V, kFusedA>), dim3(tiles_m * tiles_n),
-                     dim3(kWideThreads), kTwLdsBytes, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo,
+  hipLaunchKernelGGL((gemm_n128_kernel<V, kFusedA, kFusedB>), dim3(tiles_m * tiles_n),
+                     dim3(kWideThreads), kLds, stream, p.a_hi, p.a_lo, p.b_hi, p.b_lo,
                      p.range, static_cast<int>(p.Kp), tiles_m, tiles_n, C, ldc,
                      static_cast<int>(M), static_cast<int>(N), 1.0f / s, unscaled_only ? 1 : 0,
-                     A, lda, s);
+                     A, lda, s, B, ldb);
   return hipGetLastError();
 }
 
@@ -1043,6 +1161,25 @@ hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
   const hipError_t e = launch_el<true, true>(p, M, N, C, ldc, scale, stream, A, lda, K);
   if (e != hipSuccess) return e;
   return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
+}
+
+bool fused_split_b_ok(const float* B, int64_t ldb, int64_t N, int64_t K) {
+  return reinterpret_cast<uintptr_t>(B) % 16 == 0 && ldb % 4 == 0 && N % 4 == 0 &&
+         K % kKPad == 0 && ldb < (int64_t{1} << 22);
+}
+
+hipError_t launch_gemm_fused_b(const Planes& p, int64_t M, int64_t N, int64_t K,
+                               const float* A, int64_t lda, bool split_a_in_gemm,
+                               const float* B, int64_t ldb, float* C, int64_t ldc, float scale,
+                               hipStream_t stream) {
+  if (!fused_split_b_ok(B, ldb, N, K)) return hipErrorInvalidValue;
+  if (split_a_in_gemm) {
+    if (!fused_split_ok(A, lda, K, scale, kTermwise)) return hipErrorInvalidValue;
+    return launch_n128<kTermwise, true, true>(p, M, N, C, ldc, scale, stream, false, A, lda, B,
+                                              ldb);
+  }
+  return launch_n128<kTermwise, false, true>(p, M, N, C, ldc, scale, stream, false, nullptr, 0,
+                                             B, ldb);
 }
 
 hipError_t launch_gemm_unscaled(const Planes& p, int64_t M, int64_t N, float* C, int64_t ldc,

@@ -206,6 +206,20 @@ hipError_t launch_gemm_fused_a(const Planes& p, int64_t M, int64_t N, int64_t K,
                                const float* A, int64_t lda, float* C, int64_t ldc, float scale,
                                int variant, hipStream_t stream);
 
+// True when the termwise kernel can split B inside itself: B is 16-byte
+// aligned, ldb and N are multiples of 4 (16-byte chunks of whole columns), K
+// a multiple of 64 and 32 rows of B span less than 4 GiB.
+bool fused_split_b_ok(const float* B, int64_t ldb, int64_t N, int64_t K);
+
+// Termwise GEMM that reads B as FP32 and splits it in the kernel (requires
+// fused_split_b_ok); A is split in the kernel too when split_a_in_gemm
+// (requires fused_split_ok), else read from the A planes of the workspace.
+// The result is that of launch_gemm's termwise order on planes, bit for bit.
+hipError_t launch_gemm_fused_b(const Planes& p, int64_t M, int64_t N, int64_t K,
+                               const float* A, int64_t lda, bool split_a_in_gemm,
+                               const float* B, int64_t ldb, float* C, int64_t ldc, float scale,
+                               hipStream_t stream);
+
 // Enqueue C := 0 for an M x N block with leading dimension ldc (a fill
 // kernel, so the call stays safe under stream capture).
 hipError_t launch_zero(int64_t M, int64_t N, float* C, int64_t ldc, hipStream_t stream);

@@ -77,8 +77,15 @@ void check_validation() {
                            fake<float>(uintptr_t{1} << 39), 8192, 2048.f, 0, nullptr) == NS);
   // _ex.
   uint32_t* rep = fake<uint32_t>((uintptr_t{3} << 30) + 64);
-  CHECK(sgemm_cube_ex(4, 4, 4, A, 4, B, 4, C, 4, 2048.f, 0, 2, ws, 1 << 20, nullptr, nullptr) ==
+  CHECK(sgemm_cube_ex(4, 4, 4, A, 4, B, 4, C, 4, 2048.f, 0, 4, ws, 1 << 20, nullptr, nullptr) ==
         INV);
+  // The split of B in the GEMM: termwise only, on its layouts.
+  CHECK(sgemm_cube_ex(4, 4, 64, A, 64, B, 4, C, 4, 2048.f, 0, 2, ws, 1 << 20, nullptr, nullptr) ==
+        NS);
+  CHECK(sgemm_cube_ex(4, 6, 64, A, 64, B, 6, C, 6, 2048.f, 1, 2, ws, 1 << 20, nullptr, nullptr) ==
+        NS);
+  CHECK(sgemm_cube_ex(0, 4, 64, A, 64, B, 4, C, 4, 2048.f, 1, 2, ws, 1 << 20, nullptr, nullptr) ==
+        0);
   CHECK(sgemm_cube_ex(4, 4, 4, A, 4, B, 4, C, 4, 2048.f, 0, 0, ws, 1 << 20, rep, nullptr) == INV);
   CHECK(sgemm_cube_ex(4, 4, 4, A, 4, B, 4, C, 4, 2048.f, 0, 0, ws, 1 << 20,
                       fake<uint32_t>((uintptr_t{5} << 30) + 2), nullptr) == INV);
@@ -86,7 +93,9 @@ void check_validation() {
         0);
   CHECK(sgemm_cube_ex_workspace_size(300, 200, 100, 0, 0) ==
         sgemm_cube_workspace_size(300, 200, 100, 0));
-  CHECK(sgemm_cube_ex_workspace_size(300, 200, 100, 0, 2) == 0);
+  CHECK(sgemm_cube_ex_workspace_size(300, 200, 100, 0, 4) == 0);
+  CHECK(sgemm_cube_ex_workspace_size(300, 200, 128, 1, 2) ==
+        sgemm_cube_ex_workspace_size(300, 200, 128, 1, 0));
   // prepare / compute / compute_a / compute_stages.
   CHECK(sgemm_cube_prepare(4, 4, 4, A, 4, B, 4, 3.f, ws, need, nullptr) == INV);
   CHECK(sgemm_cube_prepare(4, 4, 4, A, 4, B, 4, 2048.f, ws, need - 1, nullptr) == INV);
@@ -96,6 +105,10 @@ void check_validation() {
   CHECK(sgemm_cube_compute_a(4, 4, 4, A, 3, C, 4, 2048.f, 0, ws, need, nullptr) == INV);
   CHECK(sgemm_cube_compute_a(4, 4, 4, A, 4, fake<float>(8), 4, 2048.f, 0, ws, need, nullptr) ==
         INV);
+  CHECK(sgemm_cube_compute_b(4, 4, 64, B, 3, C, 4, 2048.f, 1, ws, need, nullptr) == INV);
+  CHECK(sgemm_cube_compute_b(4, 4, 64, B, 4, C, 4, 2048.f, 0, ws, need, nullptr) == NS);
+  CHECK(sgemm_cube_compute_b(4, 4, 96, B, 4, C, 4, 2048.f, 1, ws, need, nullptr) == NS);
+  CHECK(sgemm_cube_compute_b(0, 4, 64, B, 4, C, 4, 2048.f, 1, ws, need, nullptr) == 0);
   CHECK(sgemm_cube_compute_stages(4, 4, 4, C, 4, 2048.f, 0, 3, ws, need, nullptr) == INV);
   CHECK(sgemm_cube_compute_stages(4, 4, 4, C, 4, 2048.f, 1, 2, ws, need, nullptr) == NS);
   // split, hgemm.

@@ -151,13 +151,14 @@ def test_hgemm_validation(lib):
 
 
 def call_ex(lib, M=4, N=4, K=4, options=0, ws=FAKE + (3 << 30), ws_bytes=1 << 20,
-            report=0, order=0):
-    return lib.sgemm_cube_ex(M, N, K, FAKE, K, FAKE + (1 << 30), N, FAKE + (2 << 30), N,
-                             2048.0, order, options, ws, ws_bytes, report, 0)
+            report=0, order=0, B=FAKE + (1 << 30), ldb=None):
+    return lib.sgemm_cube_ex(M, N, K, FAKE, K, B, N if ldb is None else ldb, FAKE + (2 << 30),
+                             N, 2048.0, order, options, ws, ws_bytes, report, 0)
 
 
 def test_ex_validation(lib):
-    assert call_ex(lib, options=2) == INVALID                     # unknown option bit
+    assert call_ex(lib, options=4) == INVALID                     # unknown option bit
+    assert call_ex(lib, options=8 | 2, order=1) == INVALID
     assert call_ex(lib, order=3) == INVALID
     assert call_ex(lib, ws_bytes=16) == INVALID                   # workspace too small
     assert call_ex(lib, ws=FAKE + (3 << 30) + 8) == INVALID       # not 256-byte aligned
@@ -168,13 +169,38 @@ def test_ex_validation(lib):
     assert call_ex(lib, M=0, options=1) == 0
 
 
+def test_ex_split_b_in_gemm_validation(lib):
+    """SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM: termwise only, without pre-scaling or a
+    range report, on B 16-byte aligned with ldb and N multiples of 4 and K a
+    multiple of 64; anything else is NOT_SUPPORTED.  M = 0 keeps the valid
+    calls free of device work."""
+    split_b = lib.OPT_SPLIT_B_IN_GEMM
+    ok = dict(M=0, N=64, K=64, options=split_b, order=1)
+    assert call_ex(lib, **ok) == 0
+    assert call_ex(lib, **{**ok, "ldb": 68}) == 0
+    assert call_ex(lib, **{**ok, "order": 0}) == NOT_SUPPORTED     # elementwise
+    assert call_ex(lib, **{**ok, "order": 2}) == NOT_SUPPORTED     # cross-terms-first
+    assert call_ex(lib, **{**ok, "options": split_b | 1}) == NOT_SUPPORTED
+    assert call_ex(lib, **{**ok, "report": FAKE + (3 << 30) - 64}) == NOT_SUPPORTED
+    assert call_ex(lib, **{**ok, "N": 66}) == NOT_SUPPORTED        # N not a multiple of 4
+    assert call_ex(lib, **{**ok, "ldb": 66}) == NOT_SUPPORTED      # ldb not a multiple of 4
+    assert call_ex(lib, **{**ok, "K": 96}) == NOT_SUPPORTED        # K not a multiple of 64
+    assert call_ex(lib, **{**ok, "B": FAKE + (1 << 30) + 4}) == NOT_SUPPORTED
+    assert call_ex(lib, **{**ok, "ldb": 1 << 22}) == NOT_SUPPORTED
+    # The other argument errors come first.
+    assert call_ex(lib, **{**ok, "ldb": 60}) == INVALID            # ldb < N
+
+
 def test_ex_workspace_size(lib):
     base = lib.sgemm_cube_workspace_size(300, 200, 100)
     assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 0) == base
     # Pre-scaling adds the row and column maxima (Mp + Np words, 256-byte rounded).
     assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 1) == base + (512 + 256) * 4
-    assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 2) == 0
+    assert lib.sgemm_cube_ex_workspace_size(300, 200, 100, 0, 4) == 0
     assert lib.sgemm_cube_ex_workspace_size(300, 200, 0, 2, 1) == 0
+    # Splitting B in the GEMM keeps the workspace of the call without it.
+    assert lib.sgemm_cube_ex_workspace_size(300, 200, 128, 1, 2) == \
+        lib.sgemm_cube_ex_workspace_size(300, 200, 128, 1, 0)
 
 
 def test_compute_stages_validation(lib):
@@ -202,6 +228,33 @@ def test_compute_tile_validation(lib):
     assert call(order=3) == INVALID
     for cfg in lib.TILE_CONFIGS:
         assert call(M=0, tm=cfg[0], tn=cfg[1], bk=cfg[2], w=cfg[3]) == 0   # validation only
+
+
+def test_compute_b_validation(lib):
+    """sgemm_cube_compute_b: the GEMM from prepared A planes and FP32 B,
+    termwise only, on the layouts the in-kernel split of B reads."""
+    B, C, ws = FAKE, FAKE + (2 << 30), FAKE + (3 << 30)
+    call = lambda M=4, N=64, K=64, B=B, ldb=None, C=C, ldc=None, scale=2048.0, order=1, ws=ws, \
+        ws_bytes=1 << 20: lib.sgemm_cube_compute_b(M, N, K, B, N if ldb is None else ldb, C,
+                                                   N if ldc is None else ldc, scale, order, ws,
+                                                   ws_bytes, 0)
+    assert call(order=3) == INVALID
+    assert call(ldb=63) == INVALID                 # ldb < N
+    assert call(ldc=63) == INVALID                 # ldc < N
+    assert call(scale=3.0) == INVALID              # not a power of two
+    assert call(B=0) == INVALID
+    assert call(C=0) == INVALID
+    assert call(C=B + 64) == INVALID               # C overlaps B
+    assert call(order=0) == NOT_SUPPORTED          # elementwise
+    assert call(order=2) == NOT_SUPPORTED          # cross-terms-first
+    assert call(N=66) == NOT_SUPPORTED             # N not a multiple of 4
+    assert call(ldb=66) == NOT_SUPPORTED           # ldb not a multiple of 4
+    assert call(K=96) == NOT_SUPPORTED             # K not a multiple of 64
+    assert call(B=B + 4) == NOT_SUPPORTED          # B not 16-byte aligned
+    assert call(ws_bytes=16) == INVALID            # workspace too small
+    assert call(ws=ws + 8) == INVALID              # not 256-byte aligned
+    assert call(M=0) == 0                          # validation only
+    assert call(N=0, B=0, ldb=1, ldc=1) == 0
 
 
 def test_compute_a_validation(lib):
