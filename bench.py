@@ -49,7 +49,9 @@ HBM_PEAK_GBS = 8000.0
 # unless some |B_hi| s exceeds 65504, in which case it does the work.  For
 # termwise the 256 x 128 kernel, likewise with A split in registers where the
 # library chooses it, and with --split-b-in-gemm the same kernel splitting B
-# (and A, where the library splits A in the GEMM) itself.
+# (and A, where the library splits A in the GEMM) itself.  The cross-terms-first
+# order has a scaled kernel and an unscaled fallback too, chosen as for the
+# elementwise order.
 GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true, true>",
                 "elementwise_unfused": "gemm_el_kernel<true, false>",
                 "elementwise_unscaled": "gemm_n128_kernel<0, false, false>",
@@ -57,7 +59,8 @@ GEMM_KERNELS = {"elementwise": "gemm_el_kernel<true, true>",
                 "termwise_fused": "gemm_n128_kernel<1, true, false>",
                 "termwise_fused_b": "gemm_n128_kernel<1, false, true>",
                 "termwise_fused_ab": "gemm_n128_kernel<1, true, true>",
-                "elementwise_cross_first": "gemm_n128_kernel<3, false, false>"}
+                "elementwise_cross_first": "gemm_n128_kernel<4, false, false>",
+                "elementwise_cross_first_unscaled": "gemm_n128_kernel<3, false, false>"}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_traffic.json")
 
 
@@ -500,16 +503,19 @@ def main():
 
     gemm_tflops = 3 * flops / (gemm_ms * 1e-3) / 1e12
     kernel_key = order
+    # The range flag: the workspace's first two words are equal after a split
+    # of B that found |B_hi| s > 65504 (s > 2^15 routes there too).
+    hdr = ws[:8].view(torch.int32).cpu()
+    unscaled = bool(hdr[0] == hdr[1]) or scale > 32768.0
     if order == "elementwise":
-        # The range flag: the workspace's first two words are equal after a
-        # split of B that found |B_hi| s > 65504 (s > 2^15 routes there too).
-        hdr = ws[:8].view(torch.int32).cpu()
-        if bool(hdr[0] == hdr[1]) or scale > 32768.0:
+        if unscaled:
             kernel_key = "elementwise_unscaled"
         elif tile:
             kernel_key = "elementwise_tile_" + tile_name(tile)
         elif not fused:
             kernel_key = "elementwise_unfused"
+    elif order == "elementwise_cross_first" and unscaled:
+        kernel_key = "elementwise_cross_first_unscaled"
     elif order == "termwise" and split_b:
         kernel_key = "termwise_fused_ab" if fused else "termwise_fused_b"
     elif order == "termwise" and fused:

@@ -536,10 +536,18 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 //     k-step.  HH goes straight into the accumulator (VGPRs) and XA_g, XB_g
 //     into block sums started from zero; one column block later,
 //     acc = (acc + XA_g / s) + XB_g / s with two v_fma_f32 (1/s is exact).
-//   kCrossFirst (the reordered elementwise accumulation proposed at the end
-//     of Sec. 4.5): per block X_g = XA_g + XB_g (one MFMA chain started from
-//     zero) and HH_g (started from zero); one column block later
-//     acc = acc + (X_g / s + HH_g) with one v_fma_f32 and one add.
+//   kCrossScaled (the reordered elementwise accumulation proposed at the end
+//     of Sec. 4.5), the scaled kernel of that order: per block one MFMA
+//     chain started from zero, XA_g, then XB_g, then A_hi (s B_hi), gives
+//     fl(X_g + s HH_g) = s fl(X_g / s + HH_g) (s a power of two, s B_hi exact
+//     under the same conditions as for the scaled elementwise kernel: s <=
+//     2^15, range flag clear; when it is set this kernel returns at once);
+//     one column block later the accumulator, which holds s * acc, adds it
+//     with one v_add_f32, and C = (s * acc) / s.
+//   kCrossFirst, its unscaled fallback (range flag set, or s > 2^15): per
+//     block X_g = XA_g + XB_g (one MFMA chain started from zero) and HH_g
+//     (started from zero); one column block later acc = acc + (X_g / s +
+//     HH_g) with one v_fma_f32 and one add.
 // In the block-fold orders the A fragments live in AGPRs (the MFMA reads its
 // A operand from there) so that the accumulators and block sums fit the
 // VGPRs; the fold of column block j runs between the MFMAs of block j+1, at
@@ -583,6 +591,9 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_hi_kernel(
 // same fragments, the same MFMAs, the same bits.  The barrier before block 7,
 // which publishes B stage kt+1, also publishes these writes; the FP32 slot
 // is refilled (stage kt+3) only after it.
+// The scaled cross-terms-first kernel: an n128 variant of the kernel only
+// (the host's order code stays kCrossFirst).
+constexpr int kCrossScaled = 4;
 constexpr int kTwM = 256;
 constexpr int kTwN = 128;
 constexpr int kTwASlot = 2 * kTwM * kStep;        // halves: A_hi, A_lo of one step
@@ -610,7 +621,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     float* __restrict__ C, int64_t ldc, int M, int N, float inv_s, int unscaled_only,
     const float* __restrict__ af, int64_t lda, float s, const float* __restrict__ bf,
     int64_t ldb) {
-  static_assert(V == kTermwise || V == kElementwise || V == kCrossFirst, "n128 variants");
+  static_assert(V == kTermwise || V == kElementwise || V == kCrossFirst || V == kCrossScaled,
+                "n128 variants");
   static_assert(!kFusedA || V == kTermwise, "the fused split of A is built for termwise only");
   static_assert(!kFusedB || V == kTermwise, "the fused split of B is built for termwise only");
   constexpr bool kFold = V != kTermwise;
@@ -629,11 +641,14 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   static_assert(kBfBase == static_cast<int>(kTwLdsBytes), "FP32 B slots follow the planes");
   static_assert(kBfBase + kTwBfSlotBytes + 3 * 4096 + 4096 <= static_cast<int>(kTwFusedBLdsBytes) &&
                     kTwFusedBLdsBytes <= kMaxLdsBytes, "FP32 B DMAs stay in LDS");
-  if constexpr (V == kElementwise) {
+  if constexpr (V == kElementwise || V == kCrossFirst) {
     // Unless the host routed the call here (unscaled_only: s is not a finite
-    // FP16 value), the scaled 256 x 256 kernel handles the case where the
-    // range flag is clear.
+    // FP16 value), the scaled kernel of the order (256 x 256 elementwise,
+    // kCrossScaled) handles the case where the range flag is clear.
     if (!unscaled_only && range[0] != range[1]) return;
+  }
+  if constexpr (V == kCrossScaled) {
+    if (range[0] == range[1]) return;  // s B_hi overflows FP16: kCrossFirst runs
   }
   extern __shared__ __align__(16) uint16_t lds[];
 
@@ -848,7 +863,12 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   }
   wait_vmcnt<0>();
   lds_barrier();
-  half8 AH[kRows], AL[kRows], NH[kRows], NL[kRows], bh[2], bl[2];
+  half8 AH[kRows], AL[kRows], NH[kRows], NL[kRows], bh[2], bl[2], bsh[2];
+  // kCrossScaled: bsh holds s B_hi of a column block (parity-indexed as bh),
+  // formed from (s, s) as a packed FP16 pair, wave-uniform.
+  const uint16_t s_bits = __builtin_bit_cast(uint16_t, static_cast<_Float16>(s));
+  const uint32_t s2 = static_cast<uint32_t>(
+      __builtin_amdgcn_readfirstlane(static_cast<int>(s_bits * 0x10001u)));
   // Fused split: F holds the FP32 fragment of one 16-row block from its reads
   // to the last split instruction that uses it; rr the residuals of two pairs.
   floatx4 F[2];
@@ -870,6 +890,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   }
   bh[0] = rd_b(0, 0, 0);
   bl[0] = rd_b(0, 1, 0);
+  if constexpr (V == kCrossScaled) bsh[0] = pk_scale(bh[0], s2);
   lds_barrier();  // A slot 0 is refilled (stage 2) during step 0
 
   // The fold of column block jp (block sums of parity cp) in two halves, for
@@ -878,6 +899,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
   //                 second acc = fl(acc + XB_g / s)
   //   cross-first   first  HH_g <- fl(X_g / s + HH_g)
   //                 second acc = fl(acc + HH_g)
+  //   cross-scaled  second s acc = fl(s acc + T_g), T_g = fl(X_g + s HH_g)
+  //                 (first: nothing)
   // One v_fma_f32 or v_add_f32 per element and half (1/s is exact).
   auto fold_first = [&](int jp, int cp, int q0, int q1) {
 #pragma unroll
@@ -895,6 +918,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
       const int i = q >> 2, e = q & 3;
       if constexpr (V == kElementwise)
         hh[i][jp][e] = __builtin_fmaf(t2[cp][i][e], inv_s, hh[i][jp][e]);
+      else if constexpr (V == kCrossScaled)
+        hh[i][jp][e] += t1[cp][i][e];
       else
         hh[i][jp][e] += t2[cp][i][e];
     }
@@ -958,6 +983,13 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
             mfma16_va_new(t1[c][i], al[i], bh[c]);
           else
             mfma16_va_new(t2[c][i], ah[i], bl[c]);
+        } else if constexpr (V == kCrossScaled) {
+          if constexpr (g == 0)
+            mfma16_va_new(t1[c][i], al[i], bh[c]);
+          else if constexpr (g == 1)
+            mfma16_va_acc(t1[c][i], ah[i], bl[c]);
+          else
+            mfma16_va_acc(t1[c][i], ah[i], bsh[c]);
         } else {
           if constexpr (g == 0)
             mfma16_va_new(t2[c][i], ah[i], bh[c]);
@@ -994,6 +1026,18 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
           if constexpr (m == 0) fold_second(jpp, c, 8, 11);
           if constexpr (m == 1) fold_second(jpp, c, 11, 14);
           if constexpr (m == 2) fold_second(jpp, c, 14, 16);
+        } else if constexpr (V == kCrossScaled) {
+          // Block jp: T_g of row i is complete after its MFMA 8 + i, so its
+          // fold may run after m >= 4 + i: rows 0-2 fold two elements after
+          // each of MFMAs 4-9, and row 3 spills into the next block's MFMAs
+          // 0-1 (that block, of parity cp, overwrites T_g of row 3 with its
+          // MFMA 3).  s B_hi of the next block: two v_pk_mul_f16 after each
+          // of MFMAs 10 and 11, 9 MFMAs ahead of its first use.
+          if constexpr (m >= 4 && m <= 9) fold_second(jp, c ^ 1, 2 * (m - 4), 2 * (m - 3));
+          constexpr int jpp = (j + kCols - 2) % kCols;
+          if constexpr (m <= 1) fold_second(jpp, c, 12 + 2 * m, 14 + 2 * m);
+          if constexpr (m == 10) pk_scale_half<0>(bsh[c ^ 1], bh[c ^ 1], s2);
+          if constexpr (m == 11) pk_scale_half<1>(bsh[c ^ 1], bh[c ^ 1], s2);
         }
         if constexpr (kFusedA) {
           // Slot P of the step: the reads of 16-row block r's two FP32
@@ -1063,13 +1107,18 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_n128_kernel(
     fold_second(kCols - 2, 0, 8, 4 * kRows);  // the spill of block 6
     fold_first(kCols - 1, 1, 0, 4 * kRows);
     fold_second(kCols - 1, 1, 0, 4 * kRows);
+  } else if constexpr (V == kCrossScaled) {
+    fold_second(kCols - 2, 0, 12, 4 * kRows);  // the spill of block 6 (row 3)
+    fold_second(kCols - 1, 1, 0, 4 * kRows);
   }
 
   const int col0 = tn * kTwN + (lane & 15);
   const int row0 = tm * kTwM + w * 64 + (lane >> 4) * 4;
   const bool full = (tm + 1) * kTwM <= M && (tn + 1) * kTwN <= N;
   store_tile16<kRows, kCols>(C, ldc, M, N, row0, col0, full, [&](int i, int j, int r) {
-    if constexpr (kFold) {
+    if constexpr (V == kCrossScaled) {
+      return hh[i][j][r] * inv_s;
+    } else if constexpr (kFold) {
       return hh[i][j][r];
     } else {
       return __builtin_fmaf(xb[i][j][r], inv_s, __builtin_fmaf(xa[i][j][r], inv_s, hh[i][j][r]));
@@ -1139,7 +1188,13 @@ hipError_t launch_gemm(const Planes& p, int64_t M, int64_t N, float* C, int64_t 
       return launch_n128<kElementwise>(p, M, N, C, ldc, scale, stream);
     }
     case kTermwise: return launch_n128<kTermwise>(p, M, N, C, ldc, scale, stream);
-    case kCrossFirst: return launch_n128<kCrossFirst>(p, M, N, C, ldc, scale, stream);
+    case kCrossFirst: {
+      if (!scaled_kernel_ok(scale))
+        return launch_n128<kCrossFirst>(p, M, N, C, ldc, scale, stream, true);
+      const hipError_t e = launch_n128<kCrossScaled>(p, M, N, C, ldc, scale, stream);
+      if (e != hipSuccess) return e;
+      return launch_n128<kCrossFirst>(p, M, N, C, ldc, scale, stream);
+    }
     case kHiOnly: return launch_hi(p, M, N, C, ldc, stream);
     default: return hipErrorInvalidValue;
   }

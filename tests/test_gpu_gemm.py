@@ -138,18 +138,23 @@ def test_non_finite_inputs_on_the_scaled_elementwise_path(gpu):
     assert np.isnan(Co).any() and np.isinf(Co).any()
 
 
+@pytest.mark.parametrize("order", ["elementwise", "elementwise_cross_first"])
 @pytest.mark.parametrize("edge", ["scaled_limit", "fallback"])
-def test_elementwise_range_switch(gpu, edge):
-    """The scaled elementwise kernel needs s * B_hi to stay finite in FP16.
-    B's largest hi exactly at 65504 / s keeps it; one FP16 ulp above switches
-    to the unscaled fallback.  Both meet the bar, on ragged shapes."""
+def test_elementwise_range_switch(gpu, edge, order):
+    """The scaled kernels of the elementwise and cross-terms-first orders need
+    s * B_hi to stay finite in FP16.  B's largest hi exactly at 65504 / s
+    keeps them; one FP16 ulp above switches to the unscaled fallback of the
+    order.  Both meet the bar and discriminate against the FP16 product, on
+    ragged shapes."""
     M, N, K = 300, 260, 257
     A, B = workloads.make_operands(M, N, K, 21, "uniform_pm1")
     B[5, 7] = 31.984375 if edge == "scaled_limit" else 32.0   # x 2^11 = 65504 or 65536
-    log(f"gemm elementwise range switch {edge}")
-    C = gemm(A, B, 2048.0, "elementwise")
-    Co = oracle.sgemm(A, B, 2048.0, "elementwise", kb=_kb())
+    log(f"gemm {order} range switch {edge}")
+    C = gemm(A, B, 2048.0, order)
+    Co = oracle.sgemm(A, B, 2048.0, order, kb=_kb())
     assert_parity(C, Co, K, abs_ab(A, B), f"range switch {edge}")
+    Ch = oracle.sgemm(A, B, 2048.0, "hi_only", kb=_kb())
+    assert_discriminates(C, Co, Ch, f"range switch {edge} {order}")
 
 
 def _range_flag(ws):
