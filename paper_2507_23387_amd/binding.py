@@ -239,11 +239,12 @@ def matmul(A, B, scale: float = 2.0**11, order="elementwise", out=None, workspac
 
 
 def matmul_ex(A, B, scale: float = 2.0**11, order="elementwise", prescale: bool = False,
-              report: bool = False, out=None):
+              report: bool = False, out=None, split_b_in_gemm: bool = False):
     """sgemm_cube_ex on the current torch stream: optional power-of-two
     pre-scaling of A's rows and B's columns; with report=True returns (C, bits)
     where bits is a one-element int32 device tensor holding the range classes
-    (RANGE_*)."""
+    (RANGE_*); split_b_in_gemm=True (termwise) sets
+    SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM."""
     import torch
 
     pa, lda = _mat(A, "A")
@@ -254,7 +255,7 @@ def matmul_ex(A, B, scale: float = 2.0**11, order="elementwise", prescale: bool 
         raise ValueError(f"shape mismatch {tuple(A.shape)} x {tuple(B.shape)}")
     C = out if out is not None else torch.empty((M, N), dtype=torch.float32, device=A.device)
     pc, ldc = _mat(C, "C")
-    options = OPT_PRESCALE if prescale else 0
+    options = (OPT_PRESCALE if prescale else 0) | (OPT_SPLIT_B_IN_GEMM if split_b_in_gemm else 0)
     n = sgemm_cube_ex_workspace_size(M, N, K, _order(order), options)
     ws = torch.empty(max(n, 256), dtype=torch.uint8, device=A.device)
     bits = torch.zeros(1, dtype=torch.int32, device=A.device) if report else None

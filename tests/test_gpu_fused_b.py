@@ -18,8 +18,8 @@ import pytest
 
 import oracle
 import workloads
-from tests.gpu_util import log, padded
-from tests.helpers import abs_ab, assert_parity
+from tests.gpu_util import log, padded, to_dev
+from tests.helpers import abs_ab, assert_discriminates, assert_parity, band_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -167,3 +167,33 @@ def test_split_b_in_gemm_larger_problem(gpu):
     rows = np.arange(0, M, 97)
     Co = oracle.sgemm_rows(A, B, rows, 2048.0, "termwise", kb=_kb())
     assert_parity(Cf[rows], Co, K, abs_ab(A[rows], B), "split B in GEMM, sampled rows")
+
+
+@pytest.mark.parametrize("name", ["c5", "c2", "c4"])
+def test_split_b_in_gemm_full_size_workloads(gpu, name):
+    """The termwise workloads at full size with B split in the GEMM kernel
+    (16384 x 1024 x 8192: A too; 4096^3 and 4096 x 4096 x 16384: A by its
+    split pass), in the launch configuration of bench.py --split-b-in-gemm.
+    C is prefilled with NaN, so the all-finite check shows every entry was
+    written; one row in every 256-row band is held to the oracle with the
+    parity bar and the discriminator against the hi-only product."""
+    import torch
+
+    from paper_2507_23387_amd import binding
+
+    w = workloads.get(name)
+    A, B = workloads.workload_operands(name)
+    scale = 2.0**11
+    log(f"split of B in the GEMM, workload {w.name}")
+    dA, dB = to_dev(A), to_dev(B)
+    Cd = torch.full((w.M, w.N), float("nan"), dtype=torch.float32, device="cuda")
+    binding.matmul_ex(dA, dB, scale, "termwise", split_b_in_gemm=True, out=Cd)
+    torch.cuda.synchronize()
+    C = Cd.cpu().numpy()
+    del dA, dB, Cd
+    assert np.isfinite(C).all()
+    rows = band_rows(w.M, w.seed + 29)
+    Co = oracle.sgemm_rows(A, B, rows, scale, "termwise", kb=_kb())
+    Ch = oracle.sgemm_rows(A, B, rows, scale, "hi_only", kb=_kb())
+    assert_parity(C[rows], Co, w.K, abs_ab(A, B, rows), f"{name} split B in GEMM")
+    assert_discriminates(C[rows], Co, Ch, f"{name} split B in GEMM")
