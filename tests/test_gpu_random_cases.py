@@ -4,7 +4,10 @@ Each case draws a shape (ragged M and N from 1 up to a few tiles, K from 40),
 leading-dimension padding, a base offset of A (aligned or not, so both the in-kernel split and
 the split pass run), a power-of-two scale from 2^0 to 2^24, an order, an entry
 point and a value distribution (uniform, normal, rows and columns moved to
-other binades, a B whose s B_hi overflows FP16).  The GPU result, written into
+other binades, a B whose s B_hi overflows FP16).  The entry points that split
+B inside the GEMM (sgemm_cube_ex with SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM,
+sgemm_cube_compute_b) take the termwise order and the layouts they need: N,
+ldb multiples of 4 and K of 64.  The GPU result, written into
 a NaN-filled C with padded ldc, must meet the parity bar against the oracle
 entry by entry, and the bytes of C outside the M x N block must be untouched.
 The cases are fixed by the seed, so a failure names a reproducible case."""
@@ -18,8 +21,9 @@ from tests.helpers import abs_ab, assert_parity
 pytestmark = pytest.mark.gpu
 
 ORDERS = ["elementwise", "termwise", "elementwise_cross_first"]
-ENTRIES = ["sgemm_cube", "ws", "noalloc", "prepare_compute", "compute_a"]
-N_CASES = 48
+ENTRIES = ["sgemm_cube", "ws", "noalloc", "prepare_compute", "compute_a", "split_b_ex",
+           "compute_b"]
+N_CASES = 63
 # The bar 2 K u32 |A||B| covers the two sides' rounding when each side's
 # rounding depth is at most K.  The elementwise order's depth is kb - 1 + 3 per
 # block (bounds.elementwise_depth; 34 for K <= 32 with the GPU's kb = 32), and
@@ -41,6 +45,11 @@ def _case(i):
     s_b = int(rng.choice([0, 6, 11, 11, 12, 13, 15, 16, 20, 24]))
     order = ORDERS[i % 3]
     entry = ENTRIES[(i // 3) % len(ENTRIES)]
+    if entry in ("split_b_ex", "compute_b"):
+        order = "termwise"
+        N = max(4, N - N % 4)
+        K = 64 * max(1, K // 64)
+        pads[1] -= pads[1] % 4
     dist = ["uniform", "normal", "binades", "overflow"][int(rng.integers(0, 4))]
     A = rng.uniform(-1, 1, (M, K)).astype(np.float32)
     B = rng.uniform(-1, 1, (K, N)).astype(np.float32)
@@ -97,6 +106,16 @@ def test_random_case_against_the_oracle(gpu, i):
             st = binding.sgemm_cube_prepare(M, N, K, a, lda, b, ldb, s, ws.data_ptr(), n, stream)
             assert st == 0
             st = binding.sgemm_cube_compute(M, N, K, cc, ldc, s, code, ws.data_ptr(), n, stream)
+        elif entry == "split_b_ex":
+            st = binding.sgemm_cube_ex(M, N, K, a, lda, b, ldb, cc, ldc, s, code,
+                                       binding.OPT_SPLIT_B_IN_GEMM, ws.data_ptr(), n, None,
+                                       stream)
+        elif entry == "compute_b":
+            st = binding.sgemm_cube_prepare(M, N, K, a, lda, None, ldb, s, ws.data_ptr(), n,
+                                            stream)
+            assert st == 0
+            st = binding.sgemm_cube_compute_b(M, N, K, b, ldb, cc, ldc, s, code, ws.data_ptr(),
+                                              n, stream)
         else:
             st = binding.sgemm_cube_prepare(M, N, K, None, lda, b, ldb, s, ws.data_ptr(), n,
                                             stream)
