@@ -1,5 +1,6 @@
 """The calls that take no stream-ordered allocation -- sgemm_cube_ws with a
-caller workspace and sgemm_cube_noalloc -- captured into a HIP graph and
+caller workspace, sgemm_cube_noalloc, and sgemm_cube_ex with the split of B
+inside the GEMM -- captured into a HIP graph and
 replayed.  The library enqueues kernels only (no memset, copy or allocation
 on the stream), so a captured call must give, on every replay, the bits of
 the same call made eagerly.  Each case is first called eagerly (which also
@@ -31,8 +32,18 @@ def _operands(M, N, K, order, seed):
     return A, B
 
 
-@pytest.mark.parametrize("entry", ["ws", "noalloc"])
-@pytest.mark.parametrize("case", CASES, ids=lambda c: f"{c[3]}-{c[0]}x{c[1]}x{c[2]}")
+# The termwise call with B split inside the GEMM (sgemm_cube_ex with
+# SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM): A split in the GEMM too (N <= 2048), and A
+# through its split pass (N > 2048).
+SPLIT_B_CASES = [(300, 204, 320, "termwise"), (130, 2100, 128, "termwise")]
+
+
+PARAMS = ([(c, e) for c in CASES for e in ("ws", "noalloc")] +
+          [(c, e) for c in SPLIT_B_CASES for e in ("ws", "noalloc", "ex_split_b")])
+
+
+@pytest.mark.parametrize("case,entry", PARAMS,
+                         ids=[f"{e}-{c[3]}-{c[0]}x{c[1]}x{c[2]}" for c, e in PARAMS])
 def test_captured_call_replays_the_eager_bits(gpu, case, entry):
     import torch
 
@@ -50,6 +61,11 @@ def test_captured_call_replays_the_eager_bits(gpu, case, entry):
             return binding.sgemm_cube_ws(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N,
                                          C.data_ptr(), N, 2048.0, code, ws.data_ptr(),
                                          ws.numel(), stream)
+        if entry == "ex_split_b":
+            return binding.sgemm_cube_ex(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N,
+                                         C.data_ptr(), N, 2048.0, code,
+                                         binding.OPT_SPLIT_B_IN_GEMM, ws.data_ptr(),
+                                         ws.numel(), None, stream)
         return binding.sgemm_cube_noalloc(M, N, K, dA.data_ptr(), K, dB.data_ptr(), N,
                                           C.data_ptr(), N, 2048.0, code, stream)
 
