@@ -13,18 +13,19 @@
 //                    k-step; on the A planes, or (kFusedA) on FP32 A that it
 //                    splits in registers (Sec. 3.3).
 //   gemm_n128_kernel 256 x 128 tiles, v_mfma_f32_16x16x32_f16: the orders
-//                    that need three accumulator sets -- termwise (Eq.
+//                    that need more than one register set -- termwise (Eq.
 //                    termwise), the unscaled elementwise fallback (range
 //                    flag set) and the cross-terms-first order (end of
-//                    Sec. 4.5); termwise also on FP32 A split in registers
-//                    (kFusedA) and on FP32 B that the workgroup splits into
-//                    its LDS planes (kFusedB).
+//                    Sec. 4.5), scaled and unscaled; termwise also on FP32
+//                    A split in registers (kFusedA) and on FP32 B that the
+//                    workgroup splits into its LDS planes (kFusedB).
 //   gemm_hi_kernel   256 x 256 tiles: HH only, the native-FP16 baseline.
 // The tile-shape sweep of the scaled elementwise order is in gemm_tile.hip.
-// For the elementwise order with s <= 2^15 both elementwise kernels are
-// launched; each reads the range flag first and the one that does not apply
-// returns at once.  For s > 2^15, which is not a finite FP16 value, the host
-// launches the unscaled kernel alone.
+// For the elementwise and cross-terms-first orders with s <= 2^15 both the
+// scaled and the unscaled kernel of the order are launched; each reads the
+// range flag first and the one that does not apply returns at once.  For s >
+// 2^15, which is not a finite FP16 value, the host launches the unscaled
+// kernel alone.
 //
 // Data path.  The planes are stored as 4 KiB tiles of 128 rows x 16 k in the
 // order and swizzle the LDS wants (internal.h), so one pipeline stage (one
