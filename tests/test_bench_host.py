@@ -144,3 +144,29 @@ def test_tile_keys_name_the_sweep_kernels():
     assert bench.tile_name((256, 256, 32, 8)) == "256x256x32x8"
     assert bench.gemm_kernel_name("elementwise_tile_256x256x32x8") == \
         "gemm_tile_kernel<256, 256, 32, 1, 2, 4>"
+
+
+def _mangled_prefix(name: str) -> bytes:
+    """Itanium-mangled form of 'kernel<args>' as it appears in the library's
+    kernel symbols: each int argument Li<n>E, each bool Lb<0|1>E."""
+    kernel, args = name.split("<", 1)
+    out = kernel + "I"
+    for a in args.rstrip(">").split(","):
+        a = a.strip()
+        out += {"true": "Lb1E", "false": "Lb0E"}.get(a, f"Li{a}E")
+    return (out + "E").encode()
+
+
+def test_roofline_kernel_names_are_kernels_of_the_library():
+    """Every kernel name bench.py reports (and keys the committed traffic
+    entries by) names a kernel the built library contains, so the rocprofv3
+    summaries and the roofline line refer to the code that runs."""
+    from paper_2507_23387_amd import binding
+
+    data = open(binding.LIB_PATH, "rb").read()
+    names = set(bench.GEMM_KERNELS.values())
+    names |= {bench.gemm_kernel_name("elementwise_tile_" + bench.tile_name(t))
+              for t in binding.TILE_CONFIGS}
+    for name in sorted(names):
+        assert _mangled_prefix(name) in data, name
+    assert _mangled_prefix("gemm_n128_kernel<5, false, false>") not in data
