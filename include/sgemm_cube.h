@@ -236,7 +236,10 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
  * reads B as FP32 and splits it itself (Sec. 3.3: the fused split, applied to
  * B; each B tile is split once per tile row of C), so B's planes are never
  * written.  Gives the same bits as sgemm_cube_ws(...) with the termwise
- * order.  Useful when one A multiplies many B.
+ * order.  On MI355X the in-kernel split costs the GEMM more than the split
+ * pass of B it replaces, so sgemm_cube_prepare(A = NULL, B) followed by
+ * sgemm_cube_compute is faster on the same A planes; this call measures that
+ * trade-off and keeps B's planes out of the workspace.
  * accum_order other than SGEMM_CUBE_TERMWISE, or B not 16-byte aligned, ldb
  * or N not a multiple of 4, K not a multiple of 64, or ldb >= 2^22 ->
  * SGEMM_CUBE_ERR_NOT_SUPPORTED.  M, N, K, B, ldb, C, ldc, scale, ws,
