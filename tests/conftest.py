@@ -9,8 +9,9 @@ if ROOT not in sys.path:
 
 
 def _ensure_built():
-    """Build the product library and the oracle only if nothing is built yet
-    (the driver and the GPU machine run the tests on what `build()` produced)."""
+    """Build the product library and the oracle only if nothing is built yet:
+    the tests run on what `__graft_entry__.build()` produced, and a source
+    change needs that build again before the tests."""
     lib = os.path.join(ROOT, "paper_2507_23387_amd", "libsgemmcube.so")
     if not os.path.exists(lib):
         from paper_2507_23387_amd import build
