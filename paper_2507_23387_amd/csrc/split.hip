@@ -17,18 +17,6 @@
 namespace sgc {
 namespace {
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-// 16-byte load of FP32 input that is read once: a non-temporal load, so the
-// input does not displace cached lines of the planes being written (the
-// tiled splits ran 7-8 % faster with it, with the last-level cache cold).
-__device__ __forceinline__ void load_stream8(const float* p, float (&v)[8]) {
-  const f32x4 a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
-  const f32x4 b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p) + 1);
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-}
-
 // Row-major split.  Thread = 4 consecutive columns of one row; blockIdx.y
 // strides over rows.  kVec: X rows are 16-byte aligned and hi/lo rows 8-byte
 // aligned, so whole quads move as float4 / 8-byte stores.
@@ -118,7 +106,10 @@ __global__ __launch_bounds__(256) void split_a_tiled_kernel(
        m < Mp; m += static_cast<int64_t>(gridDim.y) * 16) {
     float v[8];
     if (kVec && m < M && k0 + 7 < K) {
-      load_stream8(X + m * ldx + k0, v);
+      const float4* src = reinterpret_cast<const float4*>(X + m * ldx + k0);
+      const float4 f0 = src[0], f1 = src[1];
+      v[0] = f0.x; v[1] = f0.y; v[2] = f0.z; v[3] = f0.w;
+      v[4] = f1.x; v[5] = f1.y; v[6] = f1.z; v[7] = f1.w;
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? X[m * ldx + k0 + e] : 0.0f;
@@ -170,8 +161,13 @@ __global__ __launch_bounds__(256) void split_b_tiled_kernel(
   const int64_t n = panel * kPanel + nl;
   float v0[8], v1[8];
   if (kVec && k + 1 < K && n + 7 < N) {
-    load_stream8(B + k * ldb + n, v0);
-    load_stream8(B + (k + 1) * ldb + n, v1);
+    const float4* r0 = reinterpret_cast<const float4*>(B + k * ldb + n);
+    const float4* r1 = reinterpret_cast<const float4*>(B + (k + 1) * ldb + n);
+    const float4 a0 = r0[0], a1 = r0[1], c0 = r1[0], c1 = r1[1];
+    v0[0] = a0.x; v0[1] = a0.y; v0[2] = a0.z; v0[3] = a0.w;
+    v0[4] = a1.x; v0[5] = a1.y; v0[6] = a1.z; v0[7] = a1.w;
+    v1[0] = c0.x; v1[1] = c0.y; v1[2] = c0.z; v1[3] = c0.w;
+    v1[4] = c1.x; v1[5] = c1.y; v1[6] = c1.z; v1[7] = c1.w;
   } else {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
