@@ -303,12 +303,16 @@ def error_report(C_rows, A, B, rows):
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="c3")
+    ap.add_argument("--gpus", type=int, default=1,
+                    help="number of GPUs; only 1 is supported (anything else exits with a message)")
+    ap.add_argument("--steps", type=int, default=50, help="timed steps (one call each)")
+    ap.add_argument("--warmup", type=int, default=10, help="untimed steps before them")
+    ap.add_argument("--workload", default="c3",
+                    help="c1 256^3, c2 4096^3, c3 8192^3 (default), c4 4096x4096x16384, "
+                         "c5 16384x1024x8192, or a workload name")
     ap.add_argument("--order", default=None, help="elementwise | termwise | elementwise_cross_first")
-    ap.add_argument("--scale", type=float, default=None)
+    ap.add_argument("--scale", type=float, default=None,
+                    help="s, a power of two in [1, 2^24] (default: the workload's, 2^11)")
     ap.add_argument("--stages", type=int, default=0,
                     help="elementwise only: 2 = copies overlapped with the MFMAs, 1 = copies "
                          "issued and waited for at the end of each step (0 = the library's "
@@ -327,9 +331,12 @@ def main():
                          "SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM where A is split in the GEMM too)")
     ap.add_argument("--prescale", action="store_true",
                     help="time sgemm_cube_ex with power-of-two pre-scaling (one call per step)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-errors", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip timing the oracle on the host cores")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target length of the oracle's timed sample")
+    ap.add_argument("--no-errors", action="store_true",
+                    help="skip the error metrics against an FP64 product")
     ap.add_argument("--no-parity", action="store_true",
                     help="skip the comparison with the oracle (short profiling runs)")
     ap.add_argument("--no-context", action="store_true",
