@@ -10,11 +10,16 @@ sgemm_cube_compute_b) take the termwise order and the layouts they need: N,
 ldb multiples of 4 and K of 64.  The GPU result, written into
 a NaN-filled C with padded ldc, must meet the parity bar against the oracle
 entry by entry, and the bytes of C outside the M x N block must be untouched.
+A second family draws M and N from 1500 to 5000 (grids of up to 20 x 40
+tiles, over several dispatch rounds and not made of whole 16 x 16 blocks, so
+the general tile map runs): every entry of C must be written, and one row in
+every 256-row band is held to the oracle.
 The cases are fixed by the seed, so a failure names a reproducible case."""
 import numpy as np
 import pytest
 
 import oracle
+import workloads
 from tests.gpu_util import log, padded
 from tests.helpers import abs_ab, assert_parity
 
@@ -23,7 +28,8 @@ pytestmark = pytest.mark.gpu
 ORDERS = ["elementwise", "termwise", "elementwise_cross_first"]
 ENTRIES = ["sgemm_cube", "ws", "noalloc", "prepare_compute", "compute_a", "split_b_ex",
            "compute_b"]
-N_CASES = 63
+N_CASES = 252
+N_LARGE = 12
 # The bar 2 K u32 |A||B| covers the two sides' rounding when each side's
 # rounding depth is at most K.  The elementwise order's depth is kb - 1 + 3 per
 # block (bounds.elementwise_depth; 34 for K <= 32 with the GPU's kb = 32), and
@@ -51,6 +57,12 @@ def _case(i):
         K = 64 * max(1, K // 64)
         pads[1] -= pads[1] % 4
     dist = ["uniform", "normal", "binades", "overflow"][int(rng.integers(0, 4))]
+    A, B = _values(rng, M, N, K, dist, s_b)
+    return dict(M=M, N=N, K=K, pads=pads, offset=offset, s=2.0**s_b, order=order, entry=entry,
+                dist=dist, A=A, B=B)
+
+
+def _values(rng, M, N, K, dist, s_b):
     A = rng.uniform(-1, 1, (M, K)).astype(np.float32)
     B = rng.uniform(-1, 1, (K, N)).astype(np.float32)
     if dist == "normal":
@@ -62,26 +74,46 @@ def _case(i):
         B[:, ::4] *= np.float32(2.0**-8)
     elif dist == "overflow":
         B[rng.integers(0, K), rng.integers(0, N)] = np.float32(2.0**14)
-    s = 2.0**s_b
     # Keep Rule 2 (no lo overflow) and hi finite: the bar is for finite results.
     if s_b > 11:
         A *= np.float32(2.0**(11 - s_b))
         B *= np.float32(2.0**(11 - s_b))
-    return dict(M=M, N=N, K=K, pads=pads, offset=offset, s=s, order=order, entry=entry,
+    return A, B
+
+
+def _large_case(i):
+    rng = np.random.default_rng(5000 + i)
+    M = int(rng.integers(1500, 5001))
+    N = int(rng.integers(1500, 5001))
+    K = int(rng.choice([int(rng.integers(K_MIN, 600)), 64 * int(rng.integers(1, 9))]))
+    pads = [int(rng.integers(0, 6)) for _ in range(3)]
+    offset = int(rng.choice([0, 1]))
+    s_b = int(rng.choice([11, 11, 13, 16, 20]))
+    order = ORDERS[i % 3]
+    entry = ["sgemm_cube", "ws", "prepare_compute", "compute_a", "split_b_ex",
+             "compute_b"][(i // 2) % 6]
+    if entry in ("split_b_ex", "compute_b"):
+        order = "termwise"
+        N -= N % 4
+        K = 64 * max(1, K // 64)
+        pads[1] -= pads[1] % 4
+    dist = ["uniform", "normal", "overflow"][int(rng.integers(0, 3))]
+    A, B = _values(rng, M, N, K, dist, s_b)
+    return dict(M=M, N=N, K=K, pads=pads, offset=offset, s=2.0**s_b, order=order, entry=entry,
                 dist=dist, A=A, B=B)
 
 
-@pytest.mark.parametrize("i", range(N_CASES))
-def test_random_case_against_the_oracle(gpu, i):
+def _run(c, what):
+    """Call the case's entry point on a NaN-filled C with ldc = N + pads[2];
+    returns the M x N block after checking that nothing else of C changed."""
     import torch
 
     from paper_2507_23387_amd import binding
 
-    c = _case(i)
     M, N, K, s = c["M"], c["N"], c["K"], c["s"]
     lda, ldb, ldc = K + c["pads"][0], N + c["pads"][1], N + c["pads"][2]
     code = binding.ORDERS[c["order"]]
-    log(f"random case {i}: {M}x{N}x{K} lda+{c['pads'][0]} off {c['offset']} s=2^"
+    log(f"{what}: {M}x{N}x{K} lda+{c['pads'][0]} off {c['offset']} s=2^"
         f"{int(np.log2(s))} {c['order']} {c['entry']} {c['dist']}")
     _, dA = padded(c["A"], lda, offset=c["offset"])
     _, dB = padded(c["B"], ldb)
@@ -125,9 +157,31 @@ def test_random_case_against_the_oracle(gpu, i):
     assert st == 0, binding.sgemm_cube_status_string(st)
     torch.cuda.synchronize()
     full = cbuf.cpu().numpy()
-    got = full[:M * ldc].reshape(M, ldc)[:, :N]
     # Padding columns of C and anything past the last row stay NaN.
     assert np.isnan(full[:M * ldc].reshape(M, ldc)[:, N:]).all()
     assert np.isnan(full[M * ldc:]).all()
-    want = oracle.sgemm(c["A"], c["B"], s, c["order"], kb=binding.sgemm_cube_block_k())
-    assert_parity(got, want, K, abs_ab(c["A"], c["B"]), f"random case {i}")
+    return full[:M * ldc].reshape(M, ldc)[:, :N]
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_case_against_the_oracle(gpu, i):
+    from paper_2507_23387_amd import binding
+
+    c = _case(i)
+    got = _run(c, f"random case {i}")
+    want = oracle.sgemm(c["A"], c["B"], c["s"], c["order"], kb=binding.sgemm_cube_block_k())
+    assert_parity(got, want, c["K"], abs_ab(c["A"], c["B"]), f"random case {i}")
+
+
+@pytest.mark.parametrize("i", range(N_LARGE))
+def test_large_random_case_against_the_oracle(gpu, i):
+    from paper_2507_23387_amd import binding
+
+    c = _large_case(i)
+    got = _run(c, f"large random case {i}")
+    assert np.isfinite(got).all()  # every entry written (C was NaN)
+    rows = workloads.band_rows(c["M"], 7 + i)
+    want = oracle.sgemm_rows(c["A"], c["B"], rows, c["s"], c["order"],
+                             kb=binding.sgemm_cube_block_k())
+    assert_parity(got[rows], want, c["K"], abs_ab(c["A"], c["B"], rows),
+                  f"large random case {i}")
