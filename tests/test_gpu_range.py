@@ -19,7 +19,14 @@ from tests.test_oracle_range import _normal_two_word_operands
 
 pytestmark = pytest.mark.gpu
 
-ORDERS = [("elementwise", 16), ("termwise", 16), ("elementwise_cross_first", 32)]
+ORDERS = ["elementwise", "termwise", "elementwise_cross_first"]
+
+
+def _kb():
+    """The oracle's block size matching the GPU's (one 32-wide MFMA k-step)."""
+    from paper_2507_23387_amd import binding
+
+    return binding.sgemm_cube_block_k()
 
 
 def _ex(A, B, scale, order, prescale, report=False):
@@ -43,20 +50,20 @@ def _wide_range_operands(M, N, K, seed):
     return A.astype(np.float32), B.astype(np.float32)
 
 
-@pytest.mark.parametrize("order,kb", ORDERS)
+@pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("shape", [(1, 1, 1), (129, 130, 65), (300, 257, 515)],
                          ids=lambda s: "x".join(map(str, s)))
-def test_prescaled_parity(gpu, order, kb, shape):
+def test_prescaled_parity(gpu, order, shape):
     M, N, K = shape
     A, B = _wide_range_operands(M, N, K, M + N + K)
     log(f"ex prescale {order} {shape}")
     C = _ex(A, B, 2048.0, order, True)
-    Co = oracle.sgemm_prescaled(A, B, 2048.0, order, kb=kb)
+    Co = oracle.sgemm_prescaled(A, B, 2048.0, order, kb=_kb())
     assert_parity(C, Co, K, abs_ab(A, B), f"prescale {order} {shape}")
 
 
-@pytest.mark.parametrize("order,kb", ORDERS)
-def test_prescaling_is_exact_on_normal_two_word_inputs(gpu, order, kb):
+@pytest.mark.parametrize("order", ORDERS)
+def test_prescaling_is_exact_on_normal_two_word_inputs(gpu, order):
     A, B = _normal_two_word_operands(200, 190, 320, 7)
     rng = np.random.default_rng(8)
     A = np.ldexp(A, rng.integers(-6, 7, size=(200, 1)).astype(np.int32)).astype(np.float32)
@@ -96,7 +103,7 @@ def test_prescaled_subnormal_hi_workload(gpu):
     coef = float(bounds.main_bound_coef(w.K))
     assert np.all(np.abs(pre.astype(np.float64) - ref64(A, B, rows)) <= coef * abs_ab(A, B, rows))
     As, Bs = _prescaled_inputs(A, B, 2048.0)
-    Cs = oracle.sgemm_rows(As, Bs, rows, 2048.0, "termwise", kb=32)
+    Cs = oracle.sgemm_rows(As, Bs, rows, 2048.0, "termwise", kb=_kb())
     _assert_unscaled_parity(pre, Cs, A, B, rows, w.K)
 
 
@@ -156,7 +163,7 @@ def test_plain_ex_equals_sgemm_ws_and_degenerate_shapes(gpu):
 
     A, B = workloads.make_operands(130, 70, 90, 14, "normal")
     log("ex plain == ws")
-    for order, _ in ORDERS:
+    for order in ORDERS:
         C1 = binding.matmul(to_dev(A), to_dev(B), 2048.0, order)
         C2 = binding.matmul_ex(to_dev(A), to_dev(B), 2048.0, order)
         torch.cuda.synchronize()
