@@ -4,7 +4,9 @@ Each case draws a shape (ragged M and N from 1 up to a few tiles, K from 40),
 leading-dimension padding, a base offset of A (aligned or not, so both the in-kernel split and
 the split pass run), a power-of-two scale from 2^0 to 2^24, an order, an entry
 point and a value distribution (uniform, normal, rows and columns moved to
-other binades, a B whose s B_hi overflows FP16).  The entry points that split
+other binades, a B whose s B_hi overflows FP16; for sgemm_cube_ex with
+power-of-two pre-scaling, rows of A and columns of B from 2^-30 to 2^20,
+against the oracle's pre-scaled product).  The entry points that split
 B inside the GEMM (sgemm_cube_ex with SGEMM_CUBE_OPT_SPLIT_B_IN_GEMM,
 sgemm_cube_compute_b) take the termwise order and the layouts they need: N,
 ldb multiples of 4 and K of 64.  The GPU result, written into
@@ -27,8 +29,8 @@ pytestmark = pytest.mark.gpu
 
 ORDERS = ["elementwise", "termwise", "elementwise_cross_first"]
 ENTRIES = ["sgemm_cube", "ws", "noalloc", "prepare_compute", "compute_a", "split_b_ex",
-           "compute_b"]
-N_CASES = 252
+           "compute_b", "prescale_ex"]
+N_CASES = 264
 N_LARGE = 12
 # The bar 2 K u32 |A||B| covers the two sides' rounding when each side's
 # rounding depth is at most K.  The elementwise order's depth is kb - 1 + 3 per
@@ -57,6 +59,8 @@ def _case(i):
         K = 64 * max(1, K // 64)
         pads[1] -= pads[1] % 4
     dist = ["uniform", "normal", "binades", "overflow"][int(rng.integers(0, 4))]
+    if entry == "prescale_ex" and dist != "overflow":
+        dist = "wide"
     A, B = _values(rng, M, N, K, dist, s_b)
     return dict(M=M, N=N, K=K, pads=pads, offset=offset, s=2.0**s_b, order=order, entry=entry,
                 dist=dist, A=A, B=B)
@@ -74,6 +78,10 @@ def _values(rng, M, N, K, dist, s_b):
         B[:, ::4] *= np.float32(2.0**-8)
     elif dist == "overflow":
         B[rng.integers(0, K), rng.integers(0, N)] = np.float32(2.0**14)
+    elif dist == "wide":  # rows of A and columns of B from 2^-30 to 2^20 (pre-scaling)
+        A = A * np.ldexp(np.float32(1), rng.integers(-30, 21, size=(M, 1)).astype(np.int32))
+        B = B * np.ldexp(np.float32(1), rng.integers(-30, 21, size=(1, N)).astype(np.int32))
+        return A.astype(np.float32), B.astype(np.float32)
     # Keep Rule 2 (no lo overflow) and hi finite: the bar is for finite results.
     if s_b > 11:
         A *= np.float32(2.0**(11 - s_b))
@@ -142,6 +150,11 @@ def _run(c, what):
             st = binding.sgemm_cube_ex(M, N, K, a, lda, b, ldb, cc, ldc, s, code,
                                        binding.OPT_SPLIT_B_IN_GEMM, ws.data_ptr(), n, None,
                                        stream)
+        elif entry == "prescale_ex":
+            nb = binding.sgemm_cube_ex_workspace_size(M, N, K, code, binding.OPT_PRESCALE)
+            ws = torch.empty((max(nb, 1),), dtype=torch.uint8, device="cuda")
+            st = binding.sgemm_cube_ex(M, N, K, a, lda, b, ldb, cc, ldc, s, code,
+                                       binding.OPT_PRESCALE, ws.data_ptr(), nb, None, stream)
         elif entry == "compute_b":
             st = binding.sgemm_cube_prepare(M, N, K, a, lda, None, ldb, s, ws.data_ptr(), n,
                                             stream)
@@ -169,7 +182,8 @@ def test_random_case_against_the_oracle(gpu, i):
 
     c = _case(i)
     got = _run(c, f"random case {i}")
-    want = oracle.sgemm(c["A"], c["B"], c["s"], c["order"], kb=binding.sgemm_cube_block_k())
+    ref = oracle.sgemm_prescaled if c["entry"] == "prescale_ex" else oracle.sgemm
+    want = ref(c["A"], c["B"], c["s"], c["order"], kb=binding.sgemm_cube_block_k())
     assert_parity(got, want, c["K"], abs_ab(c["A"], c["B"]), f"random case {i}")
 
 
