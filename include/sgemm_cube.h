@@ -63,7 +63,10 @@ typedef enum {
 typedef enum {
   SGEMM_CUBE_OK = 0,
   SGEMM_CUBE_ERR_INVALID_VALUE = 1, /* bad dimension, stride, pointer, scale or order */
-  SGEMM_CUBE_ERR_NOT_SUPPORTED = 2, /* shape beyond the library's indexing limits */
+  SGEMM_CUBE_ERR_NOT_SUPPORTED = 2, /* shape beyond the library's indexing limits or
+                                       sgemm_cube_noalloc's fixed workspace; an option
+                                       or measurement hook used outside the orders and
+                                       layouts it covers */
   SGEMM_CUBE_ERR_ALLOC = 3,         /* workspace could not be obtained */
   SGEMM_CUBE_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed */
 } sgemm_cube_status_t;
@@ -230,6 +233,10 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
  * same M, N, K and scale as the prepare of B (the library cannot check this).
  * Afterwards the workspace's A planes are unspecified.
  */
+int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
+                         float* C, int64_t ldc, float scale, int accum_order, void* ws,
+                         size_t ws_bytes, hipStream_t stream);
+
 /*
  * The mirror image for a workspace whose A planes are prepared
  * (sgemm_cube_prepare with B == NULL), termwise order only: the GEMM kernel
@@ -249,10 +256,6 @@ int sgemm_cube_compute(int64_t M, int64_t N, int64_t K, float* C, int64_t ldc, f
  */
 int sgemm_cube_compute_b(int64_t M, int64_t N, int64_t K, const float* B, int64_t ldb,
                          float* C, int64_t ldc, float scale, int accum_order, const void* ws,
-                         size_t ws_bytes, hipStream_t stream);
-
-int sgemm_cube_compute_a(int64_t M, int64_t N, int64_t K, const float* A, int64_t lda,
-                         float* C, int64_t ldc, float scale, int accum_order, void* ws,
                          size_t ws_bytes, hipStream_t stream);
 
 /*
