@@ -170,3 +170,19 @@ def test_roofline_kernel_names_are_kernels_of_the_library():
     for name in sorted(names):
         assert _mangled_prefix(name) in data, name
     assert _mangled_prefix("gemm_n128_kernel<5, false, false>") not in data
+
+
+def test_error_report_on_a_hand_computed_case():
+    import numpy as np
+
+    # A = [[1, 2], [3, -4]], B = I: ref = A; C off by +0.5 in one entry, and a
+    # zero reference entry (excluded from the relative error).
+    A = np.array([[1.0, 2.0], [3.0, -4.0], [0.0, 0.0]], np.float32)
+    B = np.eye(2, dtype=np.float32)
+    rows = np.array([0, 1, 2])
+    C = A.copy()
+    C[1, 1] = -3.5
+    r = bench.error_report(C, A, B, rows)
+    assert r["max_rel_err"] == 0.5 / 4.0
+    assert r["max_err_over_absAabsB"] == 0.5 / 4.0
+    assert r["frobenius_rel_err"] == pytest.approx(0.5 / np.sqrt(1 + 4 + 9 + 16))
