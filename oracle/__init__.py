@@ -65,7 +65,10 @@ ORDERS = {
 DEFAULT_KB = 64  # b_k of the best block reported in Sec. 6.3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# SGEMM_CUBE_ORACLE_LIB names another build of oracle.c to load instead: the
+# planted-mistake check of the oracle's pins (tests/oracle_mutants.py) runs the
+# oracle's tests against copies with one mistake each.
+_LIB_PATH = os.environ.get("SGEMM_CUBE_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 
